@@ -1,0 +1,232 @@
+/*
+ * dcut.h -- C ABI of the D-cut verify-step library for AMD MI355X (gfx950).
+ *
+ * One speculative decoding step of D-cut (adaptive verification depth pruning
+ * for batched speculative decoding) on the target model, in four calls:
+ *
+ *   dcut_select          cross-request selection and packing   (Sec. 3.2, 3.3; Alg. 1; App. C)
+ *   dcut_verify_layer    packed ragged forward of one decoder layer (App. C packing)
+ *   dcut_lm_head_argmax  final norm, LM head and greedy argmax of every kept row
+ *   dcut_accept          greedy longest-prefix acceptance       (Sec. 3.2; App. A)
+ *
+ * Conventions shared by every call
+ *   - All pointers marked "dev" are device pointers on the current HIP device;
+ *     "host" pointers are read during the call only.  The caller owns every
+ *     buffer; the library never allocates device memory.  Scratch memory comes
+ *     from the caller through (ws, ws_bytes); dcut_workspace_bytes() gives the
+ *     size.
+ *   - Calls are asynchronous on `stream`, keep no state between calls and never
+ *     synchronise the host.  Argument errors a host can see (sizes, limits,
+ *     null pointers, budgets, costs) are rejected before any launch with
+ *     DCUT_EINVAL or DCUT_EUNSUPPORTED; a failed launch returns DCUT_EHIP.
+ *   - Faults in device-resident data never abort: they OR a DCUT_DERR_* bit
+ *     into *dev_err (when dev_err is not NULL) and the affected outputs are
+ *     unspecified, but every access stays in bounds.
+ *   - The chosen budget K* never travels to the host: kernels after dcut_select
+ *     are launched for the maximum B(D+1) rows and read K* = cu[B] on the device.
+ *   - Matrices follow PyTorch nn.Linear layout [out][in], row-major; bf16 values
+ *     are raw bits (dcut_bf16), rounded to nearest-even by the producer.
+ *   - Supported sizes: 1 <= B <= 4096, 0 <= D, D + 1 <= 64, B (D + 1) <= 8192.
+ */
+#ifndef DCUT_H
+#define DCUT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+#pragma GCC visibility push(default)
+
+typedef uint16_t dcut_bf16;
+
+enum {
+  DCUT_OK = 0,
+  DCUT_EINVAL = -1,        /* invalid argument (size, null pointer, budget, cost)   */
+  DCUT_EUNSUPPORTED = -2,  /* valid but outside what the kernels implement          */
+  DCUT_EWORKSPACE = -3,    /* ws NULL or ws_bytes below dcut_workspace_bytes()      */
+  DCUT_EHIP = -4           /* a HIP launch or runtime call failed                   */
+};
+
+/* bits OR-ed into *dev_err by the kernels */
+enum {
+  DCUT_DERR_CONF = 1,      /* a confidence is NaN, has its sign bit set, or exceeds 1 */
+  DCUT_DERR_TOKEN = 2,     /* a token id outside [0, vocab)                           */
+  DCUT_DERR_CAPACITY = 4   /* ctx_len < 0 or ctx_len + D + 1 > cap for some request   */
+};
+
+enum { DCUT_MAX_BLOCK = 64, DCUT_MAX_BATCH = 4096, DCUT_MAX_ROWS = 8192, DCUT_MAX_CANDIDATES = 64 };
+
+/*
+ * dcut_select -- score, rank, choose the budget, keep per-request prefixes, pack.
+ *
+ * Sec. 3.2 Eq. dcut-prefix-score: s_{i,0} = 1, s_{i,k} = s_{i,k-1} * c_{i,k}
+ * (one IEEE float32 multiply per depth, in depth order).  Alg. 1: the B(D+1)
+ * positions are ranked by s descending, ties to the smaller depth k, then to
+ * the smaller request index i (the order App. B states).  For every candidate
+ * budget K_r the benefit is the exact sum of u = trunc(s * 2^40) over the
+ * top-K_r positions; Sec. 3.3 Eq. dcut-objective picks r* maximising
+ * benefit_r * 2^-40 / costs[r] (float64, one IEEE division; the first strict
+ * maximum wins, so equal objectives resolve to the smaller budget).  Request i
+ * keeps its depths {0..n_i} = the kept positions (a prefix, App. A) and the
+ * kept rows are packed request by request (App. C).
+ *
+ *   B, D      batch size and drafts per request (block of D+1 positions)
+ *   conf      dev  [B][D]   float32  c_{i,1..D} in [0, 1]
+ *   draft     dev  [B][D+1] int32    z_{i,0..D}; column 0 is the bonus token
+ *   ctx_len   dev  [B]      int32    L_i, tokens already in request i's cache
+ *   R         number of candidate budgets, 1..64
+ *   budgets   host [R]      int32    non-decreasing, B <= K_r <= B(D+1)
+ *                                    (Eq. dcut-budget; see dcut_budgets_from_ratios)
+ *   costs     host [R]      double   step cost C_r of budget K_r, finite and > 0
+ *   keep_len  dev  [B]      int32    out: n_i + 1
+ *   cu        dev  [B+1]    int32    out: exclusive prefix sum of keep_len; cu[B] = K*
+ *   packed_tok, packed_pos, packed_req
+ *             dev  [B(D+1)] int32    out: row t = cu[i] + k holds z_{i,k}, L_i + k, i;
+ *                                    rows >= K* are left unspecified
+ *   choice    dev  [2]      int32    out: {K*, r*}
+ *   benefit   dev  [R]      uint64   out (nullable): sum of u over the top-K_r positions
+ *   dev_err   dev  [1]      int32    nullable; DCUT_DERR_CONF on a bad confidence
+ *                                    (the position is then scored as 0)
+ * Returns DCUT_OK, DCUT_EINVAL, DCUT_EHIP.
+ */
+int dcut_select(int B, int D, const float *conf, const int32_t *draft, const int32_t *ctx_len,
+                int R, const int32_t *budgets, const double *costs,
+                int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
+                int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                hipStream_t stream);
+
+/* Shape of one decoder layer.  n_exp == 0 selects the dense SwiGLU MLP of width
+ * `inter`; n_exp > 0 selects a routed MoE with top_k experts of width exp_inter.
+ * max_ctx bounds cap_i for every request (it sizes the attention scratch). */
+typedef struct {
+  int hidden, n_q, n_kv, head_dim;
+  int inter;
+  int n_exp, top_k, exp_inter;
+  int vocab;
+  int max_ctx;
+  float rms_eps, rope_theta;
+} dcut_layer_cfg;
+
+/* Layer weights (dev, bf16, [out][in]).  embed may be NULL when x_in is given.
+ *   w_qkv [(n_q + 2 n_kv) head_dim][hidden]: q heads, then k heads, then v heads
+ *   w_o [hidden][n_q head_dim]; w_gate_up [2 inter][hidden]: gate rows then up rows;
+ *   w_down [hidden][inter]; MoE: w_router [n_exp][hidden],
+ *   w_exp_gate_up [n_exp][2 exp_inter][hidden], w_exp_down [n_exp][hidden][exp_inter]. */
+typedef struct {
+  const dcut_bf16 *embed, *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
+  const dcut_bf16 *w_router, *w_exp_gate_up, *w_exp_down;
+} dcut_layer_w;
+
+/* Key/value cache: request i owns the slab starting at element base[i] of k and
+ * of v, laid out [n_kv][cap_i][head_dim] (keys stored after RoPE).  Slots
+ * 0..L_i-1 hold the accepted prefix. */
+typedef struct {
+  dcut_bf16 *k, *v;
+  const int64_t *base;   /* dev [B] */
+  const int32_t *cap;    /* dev [B] */
+} dcut_kv;
+
+/*
+ * dcut_verify_layer -- one pre-norm decoder layer over the K* packed rows.
+ *
+ * App. C: the kept prefixes form one contiguous batch and every kept position
+ * is scored against its request's accepted prefix.  For row t = (i, k):
+ *   x = x_in[t] (or embed[packed_tok[t]]); h = RMSNorm(x) * attn_norm;
+ *   q, k, v = h W_qkv^T; RoPE (pairs j, j + head_dim/2; angle
+ *   packed_pos[t] * rope_theta^(-2j/head_dim)) on q and k; k and v are written
+ *   to cache slot L_i + k; attention of head h over slots 0..L_i + k of kv
+ *   head h / (n_q / n_kv), scale 1/sqrt(head_dim); y = x + attn W_o^T;
+ *   out = y + MLP(RMSNorm(y) * mlp_norm), MLP = SwiGLU, or for MoE the
+ *   renormalised top_k mixture of expert SwiGLUs under softmax routing.
+ * Row results depend only on the row's own request prefix: they are bitwise
+ * identical whatever other rows are kept.
+ *
+ *   cu, packed_*  from dcut_select (dev); ctx_len dev [B]
+ *   x_in    dev [B(D+1)][hidden] float32 residual, or NULL to gather embed rows
+ *           (x_in may equal x_out)
+ *   kv      cache descriptor (the struct itself is host memory)
+ *   x_out   dev [B(D+1)][hidden] float32, out: residual after the layer (rows < K*)
+ *   dev_err DCUT_DERR_TOKEN, DCUT_DERR_CAPACITY
+ *   ws      dev scratch of dcut_workspace_bytes(1, cfg, B, D) bytes, 256-byte aligned
+ * Supported: head_dim in {64, 128}; n_q % n_kv == 0; (n_q / n_kv)(D+1) <= 256;
+ * hidden, inter, exp_inter multiples of 8.
+ */
+int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *w, int B, int D,
+                      const int32_t *cu, const int32_t *packed_tok, const int32_t *packed_pos,
+                      const int32_t *packed_req, const int32_t *ctx_len, const float *x_in,
+                      const dcut_kv *kv, float *x_out, int32_t *dev_err,
+                      void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * dcut_lm_head_argmax -- greedy target token of every kept row.
+ *
+ * f = RMSNorm(x) * final_norm (eps), logits = f W_lm^T accumulated in float32,
+ * argmax = the lowest vocabulary id among the row maxima (greedy target
+ * decoding, Sec. 4.1).  Logits are never materialised unless `logits` is given.
+ *
+ *   H, V     hidden size and vocabulary
+ *   cu       dev [B+1] from dcut_select (K* = cu[B])
+ *   x        dev [B(D+1)][H] float32 (rows < K* are read)
+ *   w_lm     dev [V][H] bf16
+ *   argmax   dev [B(D+1)] int32 out;   max_logit dev [B(D+1)] float32 out (nullable)
+ *   logits   dev [B(D+1)][V] float32 out (nullable, for checking only)
+ *   ws       dev scratch of dcut_workspace_bytes(2, cfg with hidden = H, B, D) bytes
+ * Supported: H multiple of 8.
+ */
+int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
+                        const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
+                        int32_t *argmax, float *max_logit, float *logits,
+                        void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * dcut_accept -- greedy target-only acceptance (Sec. 3.2, App. A).
+ *
+ * a_i = the largest m <= n_i such that draft[i][j] == argmax[cu[i] + j - 1]
+ * for every 1 <= j <= m; next_tok[i] = argmax[cu[i] + a_i];
+ * total = sum_i (a_i + 1), the tokens the step commits.
+ *
+ *   draft dev [B][D+1]; keep_len dev [B]; cu dev [B+1]; argmax dev [B(D+1)]
+ *   accept_len dev [B] out; next_tok dev [B] out; total dev [1] out
+ *   ctx_len_inout dev [B], nullable: incremented by a_i + 1
+ */
+int dcut_accept(int B, int D, const int32_t *draft, const int32_t *keep_len, const int32_t *cu,
+                const int32_t *argmax, int32_t *accept_len, int32_t *next_tok, int32_t *total,
+                int32_t *ctx_len_inout, hipStream_t stream);
+
+/* Scratch bytes for call `which` (0 select, 1 verify_layer, 2 lm_head_argmax,
+ * 3 accept); cfg may be NULL for 0 and 3.  Returns 0 when none is needed and
+ * (size_t)-1 for invalid shapes. */
+size_t dcut_workspace_bytes(int which, const dcut_layer_cfg *cfg, int B, int D);
+
+/* Static message for a DCUT_* status. */
+const char *dcut_strerror(int status);
+
+/* Host helper for Eq. dcut-budget: out[r] = max(B, ceil(num[r] B (D+1) / den[r]))
+ * in exact integer arithmetic, for ratios 0 <= num[r]/den[r] <= 1.  Returns
+ * DCUT_OK or DCUT_EINVAL. */
+int dcut_budgets_from_ratios(int B, int D, int R, const int32_t *num, const int32_t *den,
+                             int32_t *out);
+
+/* Host helper for the cost-table lookup of App. C: index of the captured batch
+ * size nearest to B (ties to the larger captured size), or -1 if n < 1. */
+int dcut_nearest_batch(int B, int n, const int32_t *captured);
+
+/* Kernel timing hook for profilers.  Arms `kernel` (a DCUT_KERNEL_* id) on the
+ * calling thread: its next launches on this thread record `start` before and
+ * `stop` after the kernel on the launch stream.  DCUT_KERNEL_NONE disarms. */
+enum {
+  DCUT_KERNEL_NONE = 0, DCUT_KERNEL_SELECT, DCUT_KERNEL_PACK, DCUT_KERNEL_NORM,
+  DCUT_KERNEL_GEMM_QKV, DCUT_KERNEL_ATTN, DCUT_KERNEL_ATTN_COMBINE, DCUT_KERNEL_GEMM_O,
+  DCUT_KERNEL_GEMM_GATE_UP, DCUT_KERNEL_GEMM_DOWN, DCUT_KERNEL_MOE, DCUT_KERNEL_LM_HEAD,
+  DCUT_KERNEL_ARGMAX_FINAL, DCUT_KERNEL_ACCEPT
+};
+int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop);
+
+#pragma GCC visibility pop
+#ifdef __cplusplus
+}
+#endif
+#endif /* DCUT_H */

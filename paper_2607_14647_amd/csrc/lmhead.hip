@@ -1,0 +1,58 @@
+// dcut_lm_head_argmax: final RMSNorm, LM-head GEMM with a fused row argmax.
+//
+// The GEMM epilogue reduces each row's slice of the vocabulary to one 64-bit
+// key (order-preserving logit bits << 32 | ~column) and merges it with an
+// atomic max, so the full logits are never written and the merge is
+// independent of workgroup order; the lowest column wins exact ties.
+#include "dcut_internal.h"
+
+namespace dcut {
+
+size_t lmhead_ws_bytes(int H, int B, int D) {
+  const size_t M = (size_t)B * (D + 1);
+  return align256(M * H * 2) + align256(M * sizeof(unsigned long long));
+}
+
+namespace {
+
+__global__ void __launch_bounds__(256)
+k_argmax_final(const unsigned long long *__restrict__ keys, const int32_t *__restrict__ m_count,
+               int M_max, int32_t *__restrict__ argmax, float *__restrict__ max_logit) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= M_max || t >= *m_count) return;
+  unsigned long long k = keys[t];
+  argmax[t] = (int32_t)(0xffffffffu - (uint32_t)(k & 0xffffffffu));
+  if (max_logit) {
+    uint32_t u = (uint32_t)(k >> 32);
+    u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
+    max_logit[t] = __uint_as_float(u);
+  }
+}
+
+}  // namespace
+}  // namespace dcut
+
+using namespace dcut;
+
+extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
+                                   const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
+                                   int32_t *argmax, float *max_logit, float *logits, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
+  if (!cu || !x || !final_norm || !w_lm || !argmax || !(eps >= 0.0f)) return DCUT_EINVAL;
+  const size_t need = lmhead_ws_bytes(H, B, D);
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
+  const int M = B * (D + 1);
+  uint16_t *f = (uint16_t *)ws;
+  unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)M * H * 2));
+  const int32_t *Kstar = cu + B;
+  DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x, nullptr, nullptr, 0, final_norm, eps, H, M, Kstar,
+                          nullptr, f, nullptr, 0, 0.0f, nullptr, keys, nullptr, stream));
+  GemmArgs g = {};
+  g.A = f; g.lda = H; g.K = H; g.M_max = M; g.m_count = Kstar;
+  g.W = w_lm; g.ldw = H; g.N = V;
+  g.amax_keys = keys; g.logits = logits; g.ld_logits = V;
+  DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, EPI_ARGMAX, g, stream));
+  return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3((M + 255) / 256), dim3(256), 0, stream,
+                (const unsigned long long *)keys, Kstar, M, argmax, max_logit);
+}

@@ -1,0 +1,223 @@
+// Cross-request selection (scores, ranking, budget choice, keep depths) and packing.
+//
+// Sec. 3.2 Eq. dcut-prefix-score, Sec. 3.3 Eq. dcut-objective, Alg. 1 and the
+// packing of App. C.  Both kernels run as one 1024-thread workgroup: the whole
+// problem is at most 8192 positions (64 KB of sort keys in LDS), so a single
+// workgroup avoids any grid-wide synchronisation and launch round trips.
+//
+// Bit-exactness: each request's scores are one sequential float32 product per
+// depth (denormals kept, no contraction); ranking uses the unique 64-bit key
+// (score bits, 63 - depth, 65535 - request), so any correct sort gives the same
+// order; benefits are integer sums of trunc(s * 2^40); the budget objective is
+// one float64 division.  The outputs are therefore identical on any hardware.
+#include "dcut_internal.h"
+#include "scan.h"
+
+namespace dcut {
+
+struct SelectParams {
+  int B, D, R;
+  int budgets[DCUT_MAX_CANDIDATES];
+  double costs[DCUT_MAX_CANDIDATES];
+};
+
+__device__ __forceinline__ unsigned long long rank_key(float s, int k, int i) {
+  return ((unsigned long long)__float_as_uint(s) << 32) |
+         ((unsigned long long)(63 - k) << 16) | (unsigned long long)(65535 - i);
+}
+
+// trunc(s * 2^40) for the score held in a key's upper half
+__device__ __forceinline__ unsigned long long key_units(unsigned long long key) {
+  float s = __uint_as_float((uint32_t)(key >> 32));
+  return (unsigned long long)((double)s * 1099511627776.0);
+}
+
+__device__ __forceinline__ bool conf_bad(float c) { return !(c >= 0.0f && c <= 1.0f) || signbit(c); }
+
+#pragma clang fp contract(off)
+__global__ void __launch_bounds__(1024)
+k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ keep_len,
+         int32_t *__restrict__ choice, unsigned long long *__restrict__ benefit,
+         int32_t *__restrict__ dev_err) {
+  extern __shared__ unsigned long long smem[];
+  __shared__ unsigned long long s_wave[17];
+  __shared__ unsigned long long s_ben[DCUT_MAX_CANDIDATES];
+  __shared__ unsigned long long s_tau;
+  __shared__ int s_err;
+
+  const int tid = threadIdx.x;
+  const int D = p.D, D1 = p.D + 1, B = p.B;
+  const int N = B * D1;
+  int NP = 64;
+  while (NP < N) NP <<= 1;
+  unsigned long long *keys = smem;          // [NP]
+  if (tid == 0) s_err = 0;
+
+  // 1. scores and keys, one thread per request, sequential in depth
+  for (int i = tid; i < B; i += blockDim.x) {
+    float s = 1.0f;
+    keys[i * D1] = rank_key(s, 0, i);
+    for (int k = 1; k <= D; ++k) {
+      float c = conf[(size_t)i * D + (k - 1)];
+      if (conf_bad(c)) {
+        s_err = 1;
+        c = 0.0f;
+      }
+      s = s * c;
+      keys[i * D1 + k] = rank_key(s, k, i);
+    }
+  }
+  for (int j = N + tid; j < NP; j += blockDim.x) keys[j] = 0ull;   // sorts last
+
+  // 2. bitonic sort, descending
+  for (int size = 2; size <= NP; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      for (int t = tid; t < (NP >> 1); t += blockDim.x) {
+        int lo = 2 * t - (t & (stride - 1));
+        int hi = lo + stride;
+        unsigned long long a = keys[lo], b = keys[hi];
+        bool desc = (lo & size) == 0;
+        if (desc ? (a < b) : (a > b)) {
+          keys[lo] = b;
+          keys[hi] = a;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // 3. exact prefix sums of the fixed-point scores in rank order
+  const int E = NP > (int)blockDim.x ? NP / (int)blockDim.x : 1;   // ranks per thread
+  unsigned long long local = 0;
+  for (int m = tid * E; m < tid * E + E; ++m)
+    if (m < N) local += key_units(keys[m]);
+  unsigned long long total;
+  unsigned long long pre = block_exclusive_scan(local, s_wave, &total);
+  unsigned long long *s_pre = smem + NP;    // [blockDim.x]
+  s_pre[tid] = pre;
+  __syncthreads();
+  if (tid < p.R) {
+    int K = p.budgets[tid];
+    int t = K / E, rem = K - t * E;
+    unsigned long long P = (t < (int)blockDim.x) ? s_pre[t] : total;
+    for (int m = t * E; m < t * E + rem; ++m) P += key_units(keys[m]);
+    s_ben[tid] = P;
+    if (benefit) benefit[tid] = P;
+  }
+  __syncthreads();
+
+  // 4. budget choice: first strict maximum of benefit * 2^-40 / cost
+  if (tid == 0) {
+    int best = 0;
+    double best_obj = -1.0;
+    for (int r = 0; r < p.R; ++r) {
+      double obj = ((double)s_ben[r] * 0x1p-40) / p.costs[r];
+      if (obj > best_obj) {
+        best_obj = obj;
+        best = r;
+      }
+    }
+    int Kstar = p.budgets[best];
+    choice[0] = Kstar;
+    choice[1] = best;
+    s_tau = keys[Kstar - 1];          // the K*-th largest key
+    if (s_err && dev_err) atomicOr(dev_err, DCUT_DERR_CONF);
+  }
+  __syncthreads();
+
+  // 5. keep depths: a request keeps the depths whose key ranks within the top K*
+  const unsigned long long tau = s_tau;
+  for (int i = tid; i < B; i += blockDim.x) {
+    float s = 1.0f;
+    int n = 1;                        // the bonus key (s = 1, k = 0) always ranks first in its request
+    for (int k = 1; k <= D; ++k) {
+      float c = conf[(size_t)i * D + (k - 1)];
+      if (conf_bad(c)) c = 0.0f;
+      s = s * c;
+      if (rank_key(s, k, i) >= tau) n = k + 1;
+      else break;
+    }
+    if (rank_key(1.0f, 0, i) < tau) n = 0;   // impossible when K* >= B; kept for safety
+    keep_len[i] = n;
+  }
+}
+#pragma clang fp contract(on)
+
+// Packing: cu = exclusive scan of keep_len; row t = cu[i] + k gets (z_{i,k}, L_i + k, i).
+__global__ void __launch_bounds__(1024)
+k_pack(int B, int D, const int32_t *__restrict__ keep_len, const int32_t *__restrict__ draft,
+       const int32_t *__restrict__ ctx_len, int32_t *__restrict__ cu, int32_t *__restrict__ ptok,
+       int32_t *__restrict__ ppos, int32_t *__restrict__ preq) {
+  __shared__ int s_cu[DCUT_MAX_BATCH + 1];
+  __shared__ int s_wave[17];
+  const int tid = threadIdx.x;
+  const int D1 = D + 1;
+  const int per = (B + blockDim.x - 1) / blockDim.x;   // <= 4
+  int v[4];
+  int local = 0;
+  for (int j = 0; j < per; ++j) {
+    int i = tid * per + j;
+    int kl = i < B ? keep_len[i] : 0;
+    kl = kl < 0 ? 0 : (kl > D1 ? D1 : kl);
+    v[j] = kl;
+    local += kl;
+  }
+  int total;
+  int pre = block_exclusive_scan(local, s_wave, &total);
+  for (int j = 0; j < per; ++j) {
+    int i = tid * per + j;
+    if (i < B) s_cu[i] = pre;
+    pre += v[j];
+  }
+  if (tid == 0) s_cu[B] = total;
+  __syncthreads();
+  for (int i = tid; i <= B; i += blockDim.x) cu[i] = s_cu[i];
+  for (int idx = tid; idx < B * D1; idx += blockDim.x) {
+    int i = idx / D1, k = idx - i * D1;
+    if (k < s_cu[i + 1] - s_cu[i]) {
+      int t = s_cu[i] + k;
+      ptok[t] = draft[idx];
+      ppos[t] = ctx_len[i] + k;
+      preq[t] = i;
+    }
+  }
+}
+
+}  // namespace dcut
+
+using namespace dcut;
+
+extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft,
+                           const int32_t *ctx_len, int R, const int32_t *budgets,
+                           const double *costs, int32_t *keep_len, int32_t *cu,
+                           int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
+                           int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                           hipStream_t stream) {
+  if (!batch_ok(B, D)) return DCUT_EINVAL;
+  if (R < 1 || R > DCUT_MAX_CANDIDATES || !budgets || !costs) return DCUT_EINVAL;
+  if (!conf && D > 0) return DCUT_EINVAL;
+  if (!draft || !ctx_len || !keep_len || !cu || !packed_tok || !packed_pos || !packed_req || !choice)
+    return DCUT_EINVAL;
+  SelectParams p;
+  p.B = B;
+  p.D = D;
+  p.R = R;
+  for (int r = 0; r < R; ++r) {
+    int K = budgets[r];
+    double c = costs[r];
+    if (K < B || K > B * (D + 1)) return DCUT_EINVAL;
+    if (r > 0 && K < budgets[r - 1]) return DCUT_EINVAL;
+    if (!(c > 0.0) || !(c < __builtin_inf())) return DCUT_EINVAL;
+    p.budgets[r] = K;
+    p.costs[r] = c;
+  }
+  int N = B * (D + 1), NP = 64;
+  while (NP < N) NP <<= 1;
+  size_t shmem = (size_t)(NP + 1024) * sizeof(unsigned long long);
+  DCUT_TRY(launch(DCUT_KERNEL_SELECT, k_select, dim3(1), dim3(1024), shmem, stream, p, conf,
+                  keep_len, choice, (unsigned long long *)benefit, dev_err));
+  DCUT_TRY(launch(DCUT_KERNEL_PACK, k_pack, dim3(1), dim3(1024), 0, stream, B, D,
+                  (const int32_t *)keep_len, draft, ctx_len, cu, packed_tok, packed_pos, packed_req));
+  return DCUT_OK;
+}

@@ -1,0 +1,103 @@
+"""Device-resident verify step: uploads a workload once and runs the four calls.
+
+Holds every buffer the C ABI needs (weights, KV cache, step inputs, outputs,
+workspaces) as torch device tensors and calls the library on torch's current
+stream.  No computation happens here.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import lib as L
+from . import workload as wl
+
+
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+class VerifyStep:
+    def __init__(self, cfg: wl.Config, weights: Dict[str, np.ndarray], step: Dict[str, np.ndarray],
+                 kv: Dict[str, np.ndarray], device: str = "cuda", R_max: int = 64):
+        self.cfg = cfg
+        self.B, self.D = cfg.B, cfg.D
+        self.rows = cfg.B * (cfg.D + 1)
+        ly = cfg.layer
+        self.ly = ly
+        self.device = device
+        self.w = {k: _dev(v, device) for k, v in weights.items()}
+        self.lw = L.layer_weights(self.w)
+        self.conf = _dev(step["conf"], device)
+        self.draft = _dev(step["draft"], device)
+        self.ctx_len = _dev(step["ctx_len"], device)
+        self.kv = {k: _dev(v, device) for k, v in kv.items()}
+        self.kvd = L.kv_desc(self.kv)
+        self.lcfg = L.layer_cfg(ly, int(kv["cap"].max()))
+        self.sel = L.select_outputs(self.B, self.D, R_max, device)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.dev_err = torch.zeros(1, **i32)
+        self.x = torch.zeros(self.rows, ly.hidden, dtype=torch.float32, device=device)
+        self.argmax = torch.zeros(self.rows, **i32)
+        self.max_logit = torch.zeros(self.rows, dtype=torch.float32, device=device)
+        self.accept_len = torch.zeros(self.B, **i32)
+        self.next_tok = torch.zeros(self.B, **i32)
+        self.total = torch.zeros(1, **i32)
+        self.ws_layer = L.workspace(L.workspace_bytes(1, self.lcfg, self.B, self.D), device)
+        self.ws_lm = L.workspace(L.workspace_bytes(2, self.lcfg, self.B, self.D), device)
+
+    def set_draft(self, draft: np.ndarray) -> None:
+        self.draft.copy_(torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)))
+
+    def select(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
+        L.select(self.B, self.D, self.conf, self.draft, self.ctx_len, budgets, costs, self.sel,
+                 self.dev_err)
+
+    def verify(self, x_in: Optional[torch.Tensor] = None) -> None:
+        L.verify_layer(self.lcfg, self.lw, self.B, self.D, self.sel, self.ctx_len, self.kvd, self.x,
+                       self.ws_layer, x_in=x_in, dev_err=self.dev_err)
+
+    def lm_head(self, logits: Optional[torch.Tensor] = None) -> None:
+        L.lm_head_argmax(self.ly.hidden, self.ly.vocab, self.B, self.D, self.sel["cu"], self.x,
+                         self.w["final_norm"], self.ly.rms_eps, self.w["w_lm"], self.argmax,
+                         self.ws_lm, max_logit=self.max_logit, logits=logits)
+
+    def accept(self, ctx_inout: Optional[torch.Tensor] = None) -> None:
+        L.accept(self.B, self.D, self.draft, self.sel["keep_len"], self.sel["cu"], self.argmax,
+                 self.accept_len, self.next_tok, self.total, ctx_inout)
+
+    def step(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
+        self.select(budgets, costs)
+        self.verify()
+        self.lm_head()
+        self.accept()
+
+    def host(self, name: str) -> np.ndarray:
+        src = self.sel[name] if name in self.sel else getattr(self, name)
+        return src.cpu().numpy()
+
+
+def force_drafts_on_device(st: VerifyStep, draft: np.ndarray, conf: np.ndarray,
+                           match_u: np.ndarray) -> np.ndarray:
+    """Synthetic drafter for benchmarks: z_{i,k} := the library's own greedy token at
+    position k-1 when match_u < conf (depth order, full budget each pass).
+
+    The target's greedy token at block position k-1 depends only on z_{i,0..k-1},
+    so after D passes every forced depth agrees with the verify step's argmax."""
+    B, D = st.B, st.D
+    z = np.array(draft, dtype=np.int32, copy=True)
+    full = [B * (D + 1)]
+    for k in range(1, D + 1):
+        st.set_draft(z)
+        st.select(full, [1.0])
+        st.verify()
+        st.lm_head()
+        g = st.argmax.cpu().numpy().reshape(B, D + 1)
+        hit = match_u[:, k - 1] < conf[:, k - 1]
+        z[hit, k] = g[hit, k - 1]
+    st.set_draft(z)
+    return z

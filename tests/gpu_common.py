@@ -1,0 +1,55 @@
+"""Shared helpers of the GPU parity tests (inputs from the seeded generator, expected values from the oracle)."""
+import dataclasses
+import functools
+import sys
+
+import numpy as np
+import torch
+
+from paper_2607_14647_amd import workload as wl
+
+LOGIT_RTOL = 2e-2      # max |l_gpu - l_ref| / max |l_ref| per row (bf16 path vs float64 oracle)
+ARGMAX_GAP = 1e-2      # argmax must match wherever the oracle's top-2 gap exceeds this
+X_RTOL = 2e-2          # residual rows and appended keys/values, same row-relative measure
+
+
+def need_gpu():
+    assert torch.cuda.is_available(), "these tests need an MI355X GPU"
+
+
+def note(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def tiny_variants():
+    c1 = wl.CONFIGS[1]
+    return {
+        "cfg1": c1,
+        # several 512-key chunks per request plus a ragged last chunk
+        "long": dataclasses.replace(c1, cid=81, B=12, ctx=("uniform", 500, 1600), budgets=(100,)),
+        # many row tiles, contexts down to zero
+        "wide": dataclasses.replace(c1, cid=82, B=40, ctx=("uniform", 0, 40), budgets=(300,)),
+        # block of one position (bonus only)
+        "d0": dataclasses.replace(c1, cid=83, D=0, budgets=(4,)),
+    }
+
+
+@functools.lru_cache(maxsize=8)
+def workload(cfg: wl.Config, seed: int, with_kv: bool = True):
+    st = wl.make_step_inputs(cfg, seed)
+    w = wl.make_weights(cfg, seed)
+    kv = wl.make_kv(cfg, seed, st["ctx_len"]) if with_kv else None
+    return st, w, kv
+
+
+def row_rel_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    got = got.reshape(got.shape[0], -1).astype(np.float64)
+    ref = ref.reshape(ref.shape[0], -1).astype(np.float64)
+    return np.abs(got - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-30)
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()

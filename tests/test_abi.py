@@ -1,0 +1,118 @@
+"""The C ABI without a GPU: exports, host helpers, argument validation before any launch."""
+import ctypes as C
+import json
+import os
+import re
+
+import pytest
+
+from paper_2607_14647_amd import lib as L
+from oracle import select as osel
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dcut.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(dcut_\w+)\s*\(", src, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert set(names) == set(L.EXPORTS)
+    lib = L.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_enums_match_header():
+    src = open(HEADER).read()
+    for name, val in [("DCUT_EINVAL", L.EINVAL), ("DCUT_EWORKSPACE", L.EWORKSPACE),
+                      ("DCUT_DERR_CAPACITY", L.DERR_CAPACITY)]:
+        assert re.search(rf"{name}\s*=\s*{val}\b", src)
+    ids = re.search(r"DCUT_KERNEL_NONE = 0,([^}]*)\}", src).group(1)
+    names = ["NONE"] + [s.strip().replace("DCUT_KERNEL_", "") for s in ids.split(",") if s.strip()]
+    assert names == list(L.KERNELS)
+
+
+def test_budgets_from_ratios_match_paper_and_oracle():
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "cost_table_tab3.json")))
+    for bi, B in enumerate(g["B"]):
+        assert L.budgets_from_ratios(B, g["D"], g["ratios"]) == g["budget_from_caption"][bi]
+    for B, D, n, d in [(10, 0, 1, 4), (3, 3, 1, 3), (3, 3, 1, 5), (7, 9, 2, 3), (4096, 1, 1, 3)]:
+        assert L.budgets_from_ratios(B, D, [(n, d)]) == [osel.budget_from_ratio(B, D, n, d)]
+    for bad in [[(5, 4)], [(1, 0)], [(-1, 2)]]:
+        with pytest.raises(L.DcutError):
+            L.budgets_from_ratios(8, 15, bad)
+
+
+def test_nearest_batch_rule():
+    caps = [1, 8, 16, 32, 64]
+    assert L.nearest_batch(20, caps) == 2
+    assert L.nearest_batch(24, caps) == 3          # tie 16/32 -> larger
+    assert L.nearest_batch(100, caps) == 4
+    assert L.nearest_batch(0, caps) == 0
+    assert L.nearest_batch(5, []) == -1
+
+
+def test_workspace_sizes():
+    cfg = L.LayerCfg(4096, 32, 8, 128, 14336, 0, 0, 0, 128256, 4112, 1e-5, 5e5)
+    assert L.workspace_bytes(0, None, 64, 15) == 0
+    assert L.workspace_bytes(3, None, 64, 15) == 0
+    ws1 = L.workspace_bytes(1, cfg, 64, 15)
+    assert 0 < ws1 < (1 << 31) and ws1 % 256 == 0
+    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 1024 * 8
+    assert L.workspace_bytes(1, cfg, 0, 15) == 2 ** 64 - 1
+    bad = L.LayerCfg(4096, 32, 7, 128, 14336, 0, 0, 0, 128256, 4112, 1e-5, 5e5)
+    assert L.workspace_bytes(1, bad, 64, 15) == 2 ** 64 - 1
+
+
+def _sel_call(B, D, R, budgets, costs, null_out=False):
+    lib = L.lib()
+    b = (C.c_int32 * max(R, 1))(*budgets)
+    c = (C.c_double * max(R, 1))(*costs)
+    fake = C.c_void_p(0x1000)           # never dereferenced: validation fails first
+    outp = None if null_out else fake
+    return lib.dcut_select(B, D, fake, fake, fake, R, C.cast(b, C.c_void_p), C.cast(c, C.c_void_p),
+                           outp, fake, fake, fake, fake, fake, None, None, None)
+
+
+@pytest.mark.parametrize("B,D,R,budgets,costs", [
+    (0, 15, 1, [1], [1.0]), (4097, 0, 1, [4097], [1.0]), (4, 64, 1, [4], [1.0]),
+    (1024, 15, 1, [1024], [1.0]), (4, 15, 0, [], []), (4, 15, 65, [4] * 65, [1.0] * 65),
+    (4, 15, 1, [3], [1.0]), (4, 15, 1, [65], [1.0]), (4, 15, 2, [8, 6], [1.0, 1.0]),
+    (4, 15, 1, [8], [0.0]), (4, 15, 1, [8], [-1.0]), (4, 15, 1, [8], [float("nan")]),
+    (4, 15, 1, [8], [float("inf")]),
+])
+def test_select_rejects_invalid_args(B, D, R, budgets, costs):
+    assert _sel_call(B, D, R, budgets, costs) == L.EINVAL
+
+
+def test_select_rejects_null_outputs():
+    assert _sel_call(4, 15, 1, [8], [1.0], null_out=True) == L.EINVAL
+
+
+def test_other_entry_points_reject_invalid_args():
+    lib = L.lib()
+    fake = C.c_void_p(0x1000)
+    assert lib.dcut_accept(0, 15, fake, fake, fake, fake, fake, fake, fake, None, None) == L.EINVAL
+    assert lib.dcut_accept(4, 15, None, fake, fake, fake, fake, fake, fake, None, None) == L.EINVAL
+    assert lib.dcut_lm_head_argmax(4095, 10, 4, 15, fake, fake, fake, 1e-5, fake, fake, None, None,
+                                   fake, 1 << 30, None) == L.EINVAL
+    assert lib.dcut_lm_head_argmax(4096, 10, 4, 15, fake, fake, fake, 1e-5, fake, fake, None, None,
+                                   None, 0, None) == L.EWORKSPACE
+    cfg = L.LayerCfg(256, 4, 2, 64, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
+    w = L.LayerW(*([0x1000] * 7 + [None] * 3))
+    kv = L.KV(0x1000, 0x1000, 0x1000, 0x1000)
+    args = lambda c, wsb: lib.dcut_verify_layer(C.byref(c), C.byref(w), 4, 15, fake, fake, fake, fake,
+                                                fake, None, C.byref(kv), fake, None, fake, wsb, None)
+    assert args(cfg, 0) == L.EWORKSPACE
+    bad = L.LayerCfg(256, 4, 3, 64, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
+    assert args(bad, 1 << 30) == L.EINVAL
+    hd = L.LayerCfg(256, 4, 2, 96, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
+    assert args(hd, 1 << 30) == L.EUNSUPPORTED
+    assert lib.dcut_profile_arm(99, None, None) == L.EINVAL
+    assert lib.dcut_profile_arm(L.KERNELS["LM_HEAD"], None, None) == L.EINVAL
+    assert lib.dcut_profile_arm(0, None, None) == L.OK
+    assert L.strerror(L.EHIP).startswith("HIP")
