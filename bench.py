@@ -1,0 +1,318 @@
+#!/usr/bin/env python3
+"""Benchmark of the D-cut verify step on one MI355X.
+
+A step is the whole hot path over one batch: dcut_select (scores, ranking,
+cost-model budget, keep depths, packing), dcut_verify_layer (one dense 8B-class
+decoder layer), dcut_lm_head_argmax and dcut_accept, on one stream with every
+input already resident in HBM.  The metric is accepted tokens per second:
+sum_i (a_i + 1) per step divided by the step time, at the budget K* that the
+step picks from the measured cost row.
+
+Sequence:
+  1. seeded synthetic workload (default: batch 64, dense 8B-shaped layer);
+  2. synthetic drafter: draft k matches the library's own greedy token at
+     position k-1 with probability c_k (so acceptance follows the scores);
+  3. cost row: each candidate budget K_r forced alone (R = 1), median step time;
+  4. per-kernel breakdown with the library's timing hook, to find the dominant kernel;
+  5. timed region: `--steps` adaptive steps (all candidates, measured costs),
+     with the dominant kernel timed by HIP events inside the same region;
+  6. CPU baseline: the oracle on a bounded sample of the same batch.
+Prints one JSON line.
+"""
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_work(name, cfg, K, ctx_len):
+    """Algorithmic (flops, bytes) of one launch of `name` at K kept rows."""
+    ly = cfg.layer
+    H, V, hd, nq, nkv = ly.hidden, ly.vocab, ly.head_dim, ly.n_q, ly.n_kv
+    I = ly.inter
+    nqkv = (nq + 2 * nkv) * hd
+    if name == "LM_HEAD":
+        return 2.0 * K * V * H, V * H * 2 + K * H * 2 + K * 8
+    if name == "GEMM_GATE_UP":
+        return 2.0 * K * 2 * I * H, 2 * I * H * 2 + K * H * 2 + K * I * 2
+    if name == "GEMM_DOWN":
+        return 2.0 * K * H * I, H * I * 2 + K * I * 2 + 2 * K * H * 4
+    if name == "GEMM_QKV":
+        return 2.0 * K * nqkv * H, nqkv * H * 2 + K * H * 2 + K * nqkv * 2
+    if name == "GEMM_O":
+        return 2.0 * K * H * nq * hd, H * nq * hd * 2 + K * nq * hd * 2 + 2 * K * H * 4
+    if name == "ATTN":
+        kv_bytes = float(sum(int(L) for L in ctx_len)) * nkv * hd * 2 * 2
+        return 0.0, kv_bytes + K * (nq + 2 * nkv) * hd * 2
+    return 0.0, 0.0
+
+
+def roofline(name, cfg, K, ctx_len, us):
+    fl, by = kernel_work(name, cfg, K, ctx_len)
+    if fl > 0 and fl / by > RIDGE:
+        ach = fl / (us * 1e-6) / 1e12
+        return dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=round(ach / PEAK_BF16_TFLOPS, 4), flops=fl, bytes=by)
+    ach = by / (us * 1e-6) / 1e9
+    return dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                frac=round(ach / PEAK_HBM_GBS, 4), flops=fl, bytes=by)
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_14647_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload, K):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources and the same workload and K*."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        t = json.load(open(p))
+    except ValueError:
+        return None
+    e = t.get(kernel)
+    if not e or e.get("source_hash") != source_hash() or e.get("workload") != workload or e.get("K") != K:
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, st, w, kv, budgets, costs, target_s=15.0):
+    """The oracle on the first n requests of the batch, n sized for ~10-30 s of CPU work."""
+    import numpy as np
+    import threadpoolctl
+    from oracle import accept as oacc
+    from oracle import drafts as odr
+    from oracle import layer as olay
+    from oracle import lm_head as olm
+    from oracle import select as osel
+
+    info = threadpoolctl.threadpool_info()
+    cores = max([d.get("num_threads", 1) for d in info] + [1])
+    log(f"cpu baseline: converting weights (BLAS threads {cores})")
+    w64 = olay.prepare_weights(w)
+    ly = cfg.layer
+
+    def run(sample, z):
+        t0 = time.perf_counter()
+        sel = osel.select(st["conf"], z, st["ctx_len"], budgets, costs)
+        lay = olay.verify_layer(ly, w64, kv, sel["cu"], sel["packed_tok"], sel["packed_pos"],
+                                sel["packed_req"], st["ctx_len"], cfg.D, requests=sample)
+        rows = np.concatenate([np.arange(sel["cu"][i], sel["cu"][i + 1]) for i in sample])
+        lm = olm.lm_head_argmax(lay["x_out"][rows], w64["final_norm"], ly.rms_eps, w64["w_lm"])
+        g = np.zeros(int(sel["cu"][-1]), np.int32)
+        g[rows] = lm["argmax"]
+        acc = oacc.accept(z, sel["keep_len"], sel["cu"], g)
+        dt = time.perf_counter() - t0
+        return dt, int(sum(int(acc["accept_len"][i]) + 1 for i in sample)), len(rows)
+
+    # drafts of the sampled requests forced by the oracle itself (not timed)
+    probe = [0]
+    z = odr.force_matches(ly, w64, kv, st["conf"], st["draft"], st["match_u"], st["ctx_len"], cfg.D,
+                          requests=probe)
+    dt1, _, _ = run(probe, z)
+    n = int(max(1, min(cfg.B, target_s / max(dt1, 1e-3))))
+    sample = list(range(n))
+    log(f"cpu baseline: one request {dt1:.2f}s -> sample of {n} requests; forcing their drafts")
+    z = odr.force_matches(ly, w64, kv, st["conf"], st["draft"], st["match_u"], st["ctx_len"], cfg.D,
+                          requests=sample)
+    dt, tokens, nrows = run(sample, z)
+    return dict(value=round(tokens / dt, 2), unit="accepted tokens/s", cores=int(cores), kind="oracle",
+                sample=f"requests 0..{n - 1} of the batch ({nrows} kept rows, {tokens} accepted tokens): "
+                       f"full-batch selection, then the float64 layer + LM head + accept for the sample; "
+                       f"{dt:.1f} s", seconds=round(dt, 2))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cost-reps", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold", action="store_true", help="evict the MALL between timed steps")
+    ap.add_argument("--state", default=None,
+                    help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
+                         "run of the same workload; written when missing, reused when present (a "
+                         "profiler run then sees only the timed adaptive steps at K*)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU only; the verify step has no multi-GPU path. "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_14647_amd import lib as L
+    from paper_2607_14647_amd import runner
+    from paper_2607_14647_amd import workload as wl
+
+    assert torch.cuda.is_available(), "bench.py needs an MI355X GPU"
+    cfg = wl.CONFIGS[args.config]
+    ly = cfg.layer
+    log(f"workload cfg{cfg.cid} ({cfg.name}) seed {args.seed}: generating")
+    t0 = time.time()
+    st = wl.make_step_inputs(cfg, args.seed)
+    w = wl.make_weights(cfg, args.seed)
+    kv = wl.make_kv(cfg, args.seed, st["ctx_len"])
+    log(f"generated in {time.time() - t0:.1f}s; uploading")
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    torch.cuda.synchronize()
+    budgets = list(cfg.budgets)
+    state = None
+    if args.state and os.path.exists(args.state):
+        state = json.load(open(args.state))
+        assert state["workload"] == [cfg.cid, args.seed] and state["budgets"] == budgets, "state mismatch"
+        vs.set_draft(np.array(state["draft"], dtype=np.int32))
+        log(f"reusing forced drafts, cost row and dominant kernel from {args.state}")
+    else:
+        log("forcing draft matches (synthetic drafter, D passes at full budget)")
+        runner.force_drafts_on_device(vs, st["draft"], st["conf"], st["match_u"])
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda") if args.cold else None
+
+    def timed(fn, reps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in evs:
+            if flush is not None:
+                flush.fill_(1)
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
+
+    # 3. cost row
+    cost_ms, acc_per_k = [], []
+    if state is not None:
+        cost_ms, acc_per_k = state["cost_row_ms"], state["accepted_per_budget"]
+    else:
+        log("cost row: every candidate budget alone")
+    for K in (budgets if state is None else []):
+        step = lambda K=K: vs.step([K], [1.0])
+        timed(step, 2)
+        cost_ms.append(statistics.median(timed(step, args.cost_reps)))
+        acc_per_k.append(int(vs.total.item()))
+    log("cost row (ms): " + ", ".join(f"{K}:{c:.3f}" for K, c in zip(budgets, cost_ms)))
+    adaptive = lambda: vs.step(budgets, cost_ms)
+
+    # 4. per-kernel breakdown with the timing hook
+    names = ["SELECT", "PACK", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP",
+             "GEMM_DOWN", "LM_HEAD", "ARGMAX_FINAL", "ACCEPT"]
+    breakdown = {} if state is None else state["kernel_us"]
+    for nm in (names if state is None else []):
+        pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+        for a, b in pairs:       # create the underlying events
+            a.record(stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        for a, b in pairs:
+            L.profile_arm(nm, a, b)
+            adaptive()
+        L.profile_arm("NONE")
+        torch.cuda.synchronize()
+        breakdown[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
+    dominant = max(breakdown, key=lambda k: breakdown[k])
+    if args.state and state is None:
+        json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms,
+                       accepted_per_budget=acc_per_k, kernel_us=breakdown,
+                       draft=vs.host("draft").tolist()), open(args.state, "w"))
+    log("kernel us: " + ", ".join(f"{k}={v}" for k, v in breakdown.items()) + f"; dominant {dominant}")
+
+    # 5. timed region
+    for _ in range(args.warmup):
+        adaptive()
+    torch.cuda.synchronize()
+    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in kev:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    step_ms = []
+    torch.cuda.synchronize()
+    start.record(stream)
+    for s in range(args.steps):
+        if flush is not None:
+            flush.fill_(1)
+        L.profile_arm(dominant, kev[s][0], kev[s][1])
+        adaptive()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    L.profile_arm("NONE")
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+    dom_us = 1000.0 * statistics.mean(a.elapsed_time(b) for a, b in kev)
+    Kstar, rstar = vs.host("choice").tolist()
+    accepted = int(vs.total.item())
+    assert int(vs.dev_err.item()) == 0, "device data fault"
+    value = accepted / (ms_per_step * 1e-3)
+
+    # algorithmic bytes per step (weights, KV read, KV append, packed in/out)
+    hd, nkv = ly.head_dim, ly.n_kv
+    wbytes = sum(int(w[k].size) * 2 for k in w if k != "embed") + Kstar * ly.hidden * 2
+    kvbytes = float(st["ctx_len"].astype(np.int64).sum()) * nkv * hd * 4 + Kstar * nkv * hd * 4
+    step_bytes = wbytes + kvbytes
+    workload = f"cfg{cfg.cid}"
+    rl = roofline(dominant, cfg, Kstar, st["ctx_len"], dom_us)
+    rl["traffic"] = measured_traffic(dominant, workload, Kstar)
+    rl["kernel"] = dominant
+    rl["avg_us"] = round(dom_us, 2)
+    fixed = {}
+    for rho, m in (("0.25", 4), ("0.50", 8), ("0.75", 12), ("1.00", 16)):
+        K = cfg.B * m
+        if K in budgets:
+            j = budgets.index(K)
+            fixed[rho] = dict(K=K, ms=round(cost_ms[j], 4), accepted=acc_per_k[j],
+                              tokens_per_s=round(acc_per_k[j] / (cost_ms[j] * 1e-3), 1))
+    out = dict(
+        metric="accepted tokens/s of pruned verify step (1 layer + LM head), batch 64; HBM GB/s",
+        value=round(value, 1), unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_per_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="bf16", data="synthetic",
+        config=dict(workload=f"cfg{cfg.cid} {cfg.name}: B={cfg.B}, D={cfg.D}, H={ly.hidden}, "
+                             f"{ly.n_q}q/{ly.n_kv}kv hd{ly.head_dim}, I={ly.inter}, V={ly.vocab}, "
+                             f"L~{cfg.ctx}, conf {cfg.conf_model}; seed {args.seed}",
+                    global_batch=cfg.B, K_star=Kstar, r_star=rstar, accepted_per_step=accepted,
+                    budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm"),
+        hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        step_algorithmic_bytes=int(step_bytes),
+        roofline=rl,
+        kernel_us=breakdown,
+        cost_row_ms=[round(c, 4) for c in cost_ms],
+        accepted_per_budget=acc_per_k,
+        fixed_ratio=fixed,
+        source_hash=source_hash(),
+    )
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

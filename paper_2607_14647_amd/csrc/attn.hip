@@ -40,13 +40,15 @@ __device__ __forceinline__ int n_chunks(int L, int chunk, int MC) {
   return nc > MC ? MC : nc;
 }
 
-template <int HD>
-__global__ void __launch_bounds__(1024)
+template <int HD, int NW>
+__global__ void __launch_bounds__(NW * 64)
 k_attn(AttnArgs a) {
-  constexpr int LDKs = HD + 8;      // K tile row (bf16)
-  constexpr int LDV = KT + 8;       // V^T tile row (bf16)
+  constexpr int LDKs = HD + 8;      // K tile row (bf16), 16-byte aligned rows
+  constexpr int LDV = KT + 2;       // V^T tile row (bf16): an odd number of words
   constexpr int NS = HD / 32;       // k-steps of the QK product
   constexpr int NT = HD / 16;       // 16-row tiles of O^T
+  constexpr int TOTCH = KT * (HD / 8);                 // 16-byte chunks per tile
+  constexpr int NCH = (TOTCH + NW * 64 - 1) / (NW * 64);  // per thread
   __shared__ __align__(16) uint16_t Ks[KT * LDKs];
   __shared__ __align__(16) uint16_t Vt[HD * LDV];
 
@@ -74,7 +76,6 @@ k_attn(AttnArgs a) {
   const int G = a.n_q / a.n_kv;
   const int R = G * d;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nthreads = blockDim.x;
   const int l16 = lane & 15, grp4 = lane >> 4;
 
   // this lane's query row
@@ -110,27 +111,48 @@ k_attn(AttnArgs a) {
   const size_t slab = (size_t)a.kv_base[i] + (size_t)g * cap * HD;
   const uint16_t *kbase = a.kv_k + slab;
   const uint16_t *vbase = a.kv_v + slab;
-  constexpr int CPR = HD / 8;                 // 16-byte chunks per key row
-  const int nchunk = KT * CPR;
+
+  // chunk -> (key row, column): 8 lanes cover one key's 128 contiguous bytes
+  int ckr[NCH], cc8[NCH];
+  bool cok[NCH];
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) {
+    int ch = tid + j * NW * 64;
+    cok[j] = ch < TOTCH;
+    int blk = ch >> 6, l = ch & 63;
+    ckr[j] = (blk % (KT / 8)) * 8 + (l >> 3);
+    cc8[j] = (blk / (KT / 8)) * 64 + (l & 7) * 8;
+  }
+  uint4 rk[NCH], rv[NCH];
+  auto gload = [&](int p0) {
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      int p = p0 + ckr[j];
+      if (cok[j] && p < kend) {
+        rk[j] = *(const uint4 *)(kbase + (size_t)p * HD + cc8[j]);
+        rv[j] = *(const uint4 *)(vbase + (size_t)p * HD + cc8[j]);
+      } else {
+        rk[j] = make_uint4(0, 0, 0, 0);
+        rv[j] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
 
   const int ntiles = (kend - kstart + KT - 1) / KT;
+  if (ntiles > 0) gload(kstart);
   for (int tile = 0; tile < ntiles; ++tile) {
     const int p0 = kstart + tile * KT;
     __syncthreads();
-    for (int ch = tid; ch < nchunk; ch += nthreads) {
-      int kr = ch / CPR, c8 = (ch - kr * CPR) * 8;
-      int p = p0 + kr;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (p < kend) {
-        kv = *(const uint4 *)(kbase + (size_t)p * HD + c8);
-        vv = *(const uint4 *)(vbase + (size_t)p * HD + c8);
-      }
-      *(uint4 *)(Ks + kr * LDKs + c8) = kv;
-      const uint16_t *ve = (const uint16_t *)&vv;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(c8 + e) * LDV + kr] = ve[e];
+    for (int j = 0; j < NCH; ++j) {
+      if (!cok[j]) continue;
+      *(uint4 *)(Ks + ckr[j] * LDKs + cc8[j]) = rk[j];
+      const uint16_t *ve = (const uint16_t *)&rv[j];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(cc8[j] + e) * LDV + ckr[j]] = ve[e];
     }
     __syncthreads();
+    if (tile + 1 < ntiles) gload(p0 + KT);
     if (!wave_active) continue;
 
     // S^T tiles: 4 blocks of 16 keys
@@ -191,11 +213,13 @@ k_attn(AttnArgs a) {
       const int key_a = 32 * ks + 4 * grp4;          // keys key_a..+3 and key_a+16..+3
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        const uint16_t *vp = Vt + (n * 16 + l16) * LDV;
+        const uint32_t *vp = (const uint32_t *)(Vt + (n * 16 + l16) * LDV + key_a);
         bf16x8 vf;
-        uint2 *vw = (uint2 *)&vf;
-        vw[0] = *(const uint2 *)(vp + key_a);
-        vw[1] = *(const uint2 *)(vp + key_a + 16);
+        uint32_t *vw = (uint32_t *)&vf;
+        vw[0] = vp[0];
+        vw[1] = vp[1];
+        vw[2] = vp[8];
+        vw[3] = vp[9];
         o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[n], 0, 0, 0);
       }
     }
@@ -261,7 +285,14 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
 
 template <int HD>
 int launch_hd(const AttnArgs &a, int rows_max, const int32_t *packed_req, int waves, hipStream_t s) {
-  DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD>, dim3(a.B * a.n_kv * a.max_chunks), dim3(64 * waves), 0, s, a));
+  const dim3 grid(a.B * a.n_kv * a.max_chunks);
+  if (waves <= 4) {
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 4>, grid, dim3(256), 0, s, a));
+  } else if (waves <= 8) {
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 8>, grid, dim3(512), 0, s, a));
+  } else {
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 16>, grid, dim3(1024), 0, s, a));
+  }
   int nw = rows_max * a.n_q;
   return launch(DCUT_KERNEL_ATTN_COMBINE, k_attn_combine<HD>, dim3((nw + 3) / 4), dim3(256), 0, s, a,
                 packed_req, rows_max);

@@ -38,7 +38,7 @@ ProfileHook &profile_hook();
 // Allow `kernel` to use `bytes` of dynamic LDS (needed above 64 KB); done once per kernel.
 template <typename Kernel>
 inline void allow_lds(Kernel kernel, size_t bytes) {
-  if (bytes > 65536) hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (bytes > 65536) (void)hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
 // Launch `kernel`, recording the armed profiling events around it when `kid` is armed.
@@ -78,7 +78,8 @@ enum EpiKind {
   EPI_RESID_F32 = 1,    // out_f32[m][n] += acc   (residual add, in place)
   EPI_SWIGLU = 2,       // W rows interleaved by tile: out_bf16[m][j] = SiLU(gate) * up
   EPI_QKV_ROPE = 3,     // RoPE + scatter q to out_bf16, k/v into the cache
-  EPI_ARGMAX = 4        // per-row max/argmax merged with 64-bit atomics
+  EPI_ARGMAX = 4,       // per-row max/argmax merged with 64-bit atomics
+  EPI_STORE_F32 = 5     // out_f32[m][n] = acc
 };
 
 struct GemmArgs {
@@ -102,15 +103,42 @@ struct GemmArgs {
   unsigned long long *amax_keys;  // [M_max]
   float *logits;                  // optional [M][N] float32
   long long ld_logits;
+  // split-K (EPI_RESID_F32 / EPI_STORE_F32): partial tiles [splits][M_max][N] float32
+  int splits;
+  float *split_part;
+  // grouped mode (MoE experts): row tiles come from a device list of
+  // (expert, first row, end row); W advances by w_stride elements per expert;
+  // A rows are gathered through a_rows when it is not null.
+  const int32_t *tiles;
+  const int32_t *n_tiles;
+  int m_tiles;              // grid rows of tiles (upper bound of *n_tiles)
+  long long w_stride;
+  const int32_t *a_rows;
+  int a_extent;             // rows in the A buffer (0: M_max)
 };
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s);
+// split-K factor for a residual GEMM of this shape (a function of M_max, never of K*)
+int gemm_splits(int M_max, int N, int K);
 
 // ---------------------------------------------------------------- other launchers
 int rmsnorm_launch(int kid, const float *x_in, const uint16_t *embed, const int32_t *tok, int vocab,
                    const uint16_t *gain, float eps, int H, int M_max, const int32_t *m_count,
                    float *x_copy, uint16_t *h_out, const int32_t *pos, int head_dim, float theta,
                    float2 *rope_cs, unsigned long long *amax_init, int32_t *dev_err, hipStream_t s);
+
+// Routed MoE MLP over the rows of h (bf16, [M_max][H]); adds into x_out.
+struct MoeArgs {
+  const uint16_t *h;
+  const uint16_t *w_router, *w_gate_up, *w_down;
+  int H, E, top_k, inter, M_max;
+  const int32_t *m_count;
+  float *x_out;
+  void *ws;                 // moe_ws_bytes() bytes
+};
+size_t moe_ws_bytes(int M_max, int H, int E, int top_k, int inter);
+bool moe_supported(int M_max, int H, int E, int top_k);
+int moe_launch(const MoeArgs &m, hipStream_t s);
 
 struct AttnArgs {
   const uint16_t *q;        // [M][n_q][hd] bf16 (after RoPE)

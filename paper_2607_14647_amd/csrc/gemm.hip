@@ -3,7 +3,9 @@
 // Block tile (2*WM*32) x (2*WN*32) x 64 with four waves in a 2 x 2 grid; every
 // wave owns WM x WN tiles of v_mfma_f32_32x32x16_bf16 (float32 accumulators).
 // Operands go global -> registers -> LDS (double buffered, 16-byte padded rows),
-// with the next k-slice loaded while the current one is multiplied.
+// with the next k-slice loaded while the current one is multiplied.  Residual
+// GEMMs with few output tiles split K over gridDim.y (a factor fixed by the
+// shape); k_splitk_reduce then adds the partial tiles in split order.
 //
 // Rows: the grid covers M_max rows; the live row count M (K*) is read on the
 // device and whole row tiles beyond it exit at once.  The tile shape never
@@ -32,6 +34,7 @@ __device__ __forceinline__ uint32_t orderable(float v) {
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
 
 // W row feeding logical tile column group `grp` (global, 32 columns each), plus
 // the first output column of that group; returns -1 when the group is past N.
@@ -64,25 +67,33 @@ template <int EPI, int WM, int WN>
 __global__ void __launch_bounds__(256)
 k_gemm(GemmArgs a) {
   constexpr int TM = 64 * WM, TN = 64 * WN;
-  constexpr int ACH = TM * TK / 8 / 256;    // 16-byte A chunks per thread
-  constexpr int BCH = TN * TK / 8 / 256;
-  extern __shared__ __align__(16) uint16_t lds[];
-  uint16_t *As = lds;                        // [2][TM][LDK]
-  uint16_t *Bs = lds + 2 * TM * LDK;         // [2][TN][LDK]
+  extern __shared__ __align__(16) uint16_t lds[];   // [2][TM][LDK] (A) then [2][TN][LDK] (B)
 
-  const int M = *a.m_count;
-  const int nMT = (a.M_max + TM - 1) / TM;
+  int M = *a.m_count;
+  const int nMT = a.m_tiles > 0 ? a.m_tiles : (a.M_max + TM - 1) / TM;
   const int total = gridDim.x;
   const int per = total >> 3;
   const int w = blockIdx.x;
   const int id = (w < per * 8) ? (w & 7) * per + (w >> 3) : w;
   const int mt = id % nMT, nt = id / nMT;
-  const int m0 = mt * TM;
+  int m0 = mt * TM;
+  const uint16_t *Wb = a.W;
+  if (a.tiles) {
+    if (mt >= *a.n_tiles) return;
+    const int e = a.tiles[3 * mt];
+    m0 = a.tiles[3 * mt + 1];
+    M = a.tiles[3 * mt + 2];
+    Wb += (size_t)e * a.w_stride;
+  }
   if (m0 >= M) return;
   const int grp0 = nt * (TN / 32);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  constexpr int ACH = TM * TK / 8 / 256;    // 16-byte A chunks per thread
+  constexpr int BCH = TN * TK / 8 / 256;
+  uint16_t *As = lds;                        // [2][TM][LDK]
+  uint16_t *Bs = lds + 2 * TM * LDK;         // [2][TN][LDK]
 
   // per-thread load descriptors
   const uint16_t *aptr[ACH];
@@ -95,7 +106,9 @@ k_gemm(GemmArgs a) {
     acol[j] = (c & 7) * 8;
     int gm = m0 + arow[j];
     aval[j] = gm < M;
-    aptr[j] = a.A + (size_t)(aval[j] ? gm : 0) * a.lda + acol[j];
+    int src = aval[j] ? gm : 0;
+    if (a.a_rows && aval[j]) src = a.a_rows[gm];
+    aptr[j] = a.A + (size_t)src * a.lda + acol[j];
   }
   const uint16_t *bptr[BCH];
   bool bval[BCH];
@@ -111,17 +124,25 @@ k_gemm(GemmArgs a) {
     if (EPI == EPI_SWIGLU) ok = ok && ((((grp0 + (brow[j] >> 5)) >> 1) * 32 + (brow[j] & 31)) < a.swiglu_inter);
     else ok = ok && r < a.N;
     bval[j] = ok;
-    bptr[j] = a.W + (size_t)(ok ? r : 0) * a.ldw + bcol[j];
+    bptr[j] = Wb + (size_t)(ok ? r : 0) * a.ldw + bcol[j];
   }
 
+  // the next k-slice is loaded into registers while the current one is multiplied
   uint4 ra[ACH], rb[BCH];
-  auto gload = [&](int k0) {
+  auto gload = [&](int kt) {
+    const int k0 = kt * TK;
 #pragma unroll
-    for (int j = 0; j < ACH; ++j)
-      ra[j] = (aval[j] && k0 + acol[j] < a.K) ? *(const uint4 *)(aptr[j] + k0) : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < ACH; ++j) {
+      const bool ok = aval[j] && k0 + acol[j] < a.K;
+      const uint4 v = *(const uint4 *)(aptr[j] + (ok ? k0 : 0));
+      ra[j] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
 #pragma unroll
-    for (int j = 0; j < BCH; ++j)
-      rb[j] = (bval[j] && k0 + bcol[j] < a.K) ? *(const uint4 *)(bptr[j] + k0) : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < BCH; ++j) {
+      const bool ok = bval[j] && k0 + bcol[j] < a.K;
+      const uint4 v = *(const uint4 *)(bptr[j] + (ok ? k0 : 0));
+      rb[j] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
   };
   auto lstore = [&](int buf) {
     uint16_t *as = As + buf * TM * LDK;
@@ -140,14 +161,20 @@ k_gemm(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = (a.K + TK - 1) / TK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
   const int l32 = lane & 31, khalf = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * TK);
+  // this workgroup's k range (split-K over gridDim.y, fixed by the shape)
+  const int nk_all = (a.K + TK - 1) / TK;
+  const int per_split = (nk_all + (int)gridDim.y - 1) / (int)gridDim.y;
+  const int kt0 = (int)blockIdx.y * per_split;
+  const int nk = max(0, min(nk_all, kt0 + per_split) - kt0);
+  if (nk > 0) {
+    gload(kt0);
+    lstore(0);
+    __syncthreads();
+  }
+  for (int it = 0; it < nk; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nk) gload(kt0 + it + 1);
     const uint16_t *as = As + buf * TM * LDK + (wm * WM * 32 + l32) * LDK + khalf;
     const uint16_t *bs = Bs + buf * TN * LDK + (wn * WN * 32 + l32) * LDK + khalf;
 #pragma unroll
@@ -163,14 +190,33 @@ k_gemm(GemmArgs a) {
         for (int j = 0; j < WN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
+    if (it + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
+  }
+
+  if (gridDim.y > 1) {
+    // split-K partial tile; k_splitk_reduce applies the epilogue in split order
+    float *part = a.split_part + (size_t)blockIdx.y * a.M_max * a.N;
+    const int rb_ = m0 + wm * WM * 32 + 4 * (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) {
+        int col = (grp0 + wn * WN + j) * 32 + l32;
+        if (col >= a.N) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int gm = rb_ + i * 32 + 8 * (r >> 2) + (r & 3);
+          if (gm < M) part[(size_t)gm * a.N + col] = acc[i][j][r];
+        }
+      }
+    return;
   }
 
   // ------------------------------------------------------------ epilogues
   // accumulator element r of a 32x32 tile: row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
   const int rbase = m0 + wm * WM * 32 + 4 * (lane >> 5);
-  if (EPI == EPI_STORE_BF16 || EPI == EPI_RESID_F32) {
+  if (EPI == EPI_STORE_BF16 || EPI == EPI_RESID_F32 || EPI == EPI_STORE_F32) {
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -184,6 +230,7 @@ k_gemm(GemmArgs a) {
           int gm = rbase + i * 32 + 8 * (r >> 2) + (r & 3);
           if (gm >= M) continue;
           if (EPI == EPI_STORE_BF16) a.out_bf16[(size_t)gm * a.ldo + col] = f2bf(acc[i][j][r]);
+          else if (EPI == EPI_STORE_F32) a.out_f32[(size_t)gm * a.ldo + col] = acc[i][j][r];
           else {
             float *o = a.out_f32 + (size_t)gm * a.ldo + col;
             *o = *o + acc[i][j][r];
@@ -273,17 +320,57 @@ k_gemm(GemmArgs a) {
   }
 }
 
+// out[m][n] (+)= sum over splits of part[s][m][n], in split order (rows m < K*).
+__global__ void __launch_bounds__(256)
+k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
+                const int32_t *__restrict__ m_count, float *__restrict__ out, int ldo, int accumulate) {
+  const int m = blockIdx.y;
+  if (m >= *m_count) return;
+  const int n = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (n >= N) return;
+  float4 acc = *(const float4 *)(part + (size_t)m * N + n);
+  for (int s = 1; s < splits; ++s) {
+    float4 v = *(const float4 *)(part + ((size_t)s * M_max + m) * N + n);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  float4 *o = (float4 *)(out + (size_t)m * ldo + n);
+  if (accumulate) {
+    float4 x = *o;
+    acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
+  }
+  *o = acc;
+}
+
 template <int EPI, int WM, int WN>
 int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   constexpr int TM = 64 * WM, TN = 64 * WN;
   int ncols = (EPI == EPI_SWIGLU) ? 2 * a.swiglu_inter : a.N;
-  int nMT = (a.M_max + TM - 1) / TM;
+  int nMT = a.m_tiles > 0 ? a.m_tiles : (a.M_max + TM - 1) / TM;
   int nNT = (EPI == EPI_SWIGLU) ? (a.swiglu_inter + TN / 2 - 1) / (TN / 2) : (ncols + TN - 1) / TN;
   size_t shmem = (size_t)2 * (TM + TN) * LDK * sizeof(uint16_t);
+  const int splits = a.splits > 1 ? a.splits : 1;
+  if (splits > 1) {
+    if ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32) || a.tiles || !a.split_part || a.N % 4 || a.ldo % 4)
+      return DCUT_EINVAL;
+    DCUT_TRY(launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT, splits), dim3(256), shmem, s, a));
+    return launch(DCUT_KERNEL_NONE, k_splitk_reduce, dim3((a.N + 1023) / 1024, a.M_max), dim3(256), 0, s,
+                  (const float *)a.split_part, splits, a.M_max, a.N, a.m_count, a.out_f32, a.ldo,
+                  EPI == EPI_RESID_F32 ? 1 : 0);
+  }
   return launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT), dim3(256), shmem, s, a);
 }
 
 }  // namespace
+
+int gemm_splits(int M_max, int N, int K) {
+  const int nMT = (M_max + 127) / 128, nNT = (N + 127) / 128;
+  const int nk = (K + TK - 1) / TK;
+  int sp = (1024 + nMT * nNT - 1) / (nMT * nNT);
+  const int cap = nk / 8 > 1 ? nk / 8 : 1;      // keep at least 8 k-slices per split
+  if (sp > cap) sp = cap;
+  if (sp > 16) sp = 16;
+  return sp < 1 ? 1 : sp;
+}
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {
   switch (epi) {
@@ -292,6 +379,7 @@ int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {
     case EPI_SWIGLU: return launch_tile<EPI_SWIGLU, 2, 2>(kid, a, s);
     case EPI_QKV_ROPE: return launch_tile<EPI_QKV_ROPE, 2, 2>(kid, a, s);
     case EPI_ARGMAX: return launch_tile<EPI_ARGMAX, 2, 2>(kid, a, s);
+    case EPI_STORE_F32: return launch_tile<EPI_STORE_F32, 2, 2>(kid, a, s);
   }
   return DCUT_EINVAL;
 }

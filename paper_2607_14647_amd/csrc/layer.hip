@@ -19,7 +19,8 @@ namespace dcut {
 constexpr int ATTN_CHUNK = 512;
 
 struct LayerWs {
-  size_t h, q, attn, rope, part, mid, moe, total;
+  size_t h, q, attn, rope, part, mid, split, moe, total;
+  int split_o, split_down;
 };
 
 static bool layer_cfg_ok(const dcut_layer_cfg *c, int B, int D) {
@@ -34,10 +35,10 @@ static bool layer_cfg_ok(const dcut_layer_cfg *c, int B, int D) {
   return true;
 }
 
-static bool layer_cfg_supported(const dcut_layer_cfg *c, int D) {
+static bool layer_cfg_supported(const dcut_layer_cfg *c, int B, int D) {
   if (c->head_dim != 64 && c->head_dim != 128) return false;
   if ((c->n_q / c->n_kv) * (D + 1) > 256) return false;
-  if (c->n_exp > 0) return false;   // routed MoE MLP is not built yet
+  if (c->n_exp > 0 && !moe_supported(B * (D + 1), c->hidden, c->n_exp, c->top_k)) return false;
   return true;
 }
 
@@ -53,7 +54,12 @@ static LayerWs layer_ws(const dcut_layer_cfg *c, int B, int D) {
   w.rope = off; off = align256(off + M * (c->head_dim / 2) * sizeof(float2));
   w.part = off; off = align256(off + M * c->n_q * (size_t)mc * (c->head_dim + 2) * sizeof(float));
   w.mid = off; off = align256(off + (c->n_exp == 0 ? M * (size_t)c->inter * 2 : 0));
+  w.split_o = gemm_splits((int)M, c->hidden, (int)qd);
+  w.split_down = c->n_exp == 0 ? gemm_splits((int)M, c->hidden, c->inter) : 1;
+  const int sp = w.split_o > w.split_down ? w.split_o : w.split_down;
+  w.split = off; off = align256(off + (sp > 1 ? (size_t)sp * M * c->hidden * sizeof(float) : 0));
   w.moe = off;
+  if (c->n_exp > 0) off = align256(off + moe_ws_bytes((int)M, c->hidden, c->n_exp, c->top_k, c->exp_inter));
   w.total = off;
   return w;
 }
@@ -80,7 +86,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   if (!x_in && !w->embed) return DCUT_EINVAL;
   if (cfg->n_exp == 0 && (!w->w_gate_up || !w->w_down)) return DCUT_EINVAL;
   if (cfg->n_exp > 0 && (!w->w_router || !w->w_exp_gate_up || !w->w_exp_down)) return DCUT_EINVAL;
-  if (!layer_cfg_supported(cfg, D)) return DCUT_EUNSUPPORTED;
+  if (!layer_cfg_supported(cfg, B, D)) return DCUT_EUNSUPPORTED;
   const LayerWs L = layer_ws(cfg, B, D);
   if (!ws || ws_bytes < L.total || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
 
@@ -91,6 +97,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   float2 *rope = (float2 *)(base + L.rope);
   float *part = (float *)(base + L.part);
   uint16_t *mid = (uint16_t *)(base + L.mid);
+  float *split = (float *)(base + L.split);
 
   const int H = cfg->hidden, hd = cfg->head_dim, nq = cfg->n_q, nkv = cfg->n_kv;
   const int M = B * (D + 1);
@@ -122,11 +129,19 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   o.A = att; o.lda = nq * hd; o.K = nq * hd; o.M_max = M; o.m_count = Kstar;
   o.W = w->w_o; o.ldw = nq * hd; o.N = H;
   o.out_f32 = x_out; o.ldo = H;
+  o.splits = L.split_o; o.split_part = split;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_O, EPI_RESID_F32, o, stream));
   // 5. norm2
   DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x_out, nullptr, nullptr, 0, w->mlp_norm, cfg->rms_eps, H,
                           M, Kstar, nullptr, h, nullptr, 0, 0.0f, nullptr, nullptr, dev_err, stream));
   // 6. MLP
+  if (cfg->n_exp > 0) {
+    MoeArgs me = {};
+    me.h = h; me.w_router = w->w_router; me.w_gate_up = w->w_exp_gate_up; me.w_down = w->w_exp_down;
+    me.H = H; me.E = cfg->n_exp; me.top_k = cfg->top_k; me.inter = cfg->exp_inter; me.M_max = M;
+    me.m_count = Kstar; me.x_out = x_out; me.ws = base + L.moe;
+    return moe_launch(me, stream);
+  }
   GemmArgs gu = {};
   gu.A = h; gu.lda = H; gu.K = H; gu.M_max = M; gu.m_count = Kstar;
   gu.W = w->w_gate_up; gu.ldw = H; gu.N = 2 * cfg->inter; gu.swiglu_inter = cfg->inter;
@@ -136,6 +151,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   dn.A = mid; dn.lda = cfg->inter; dn.K = cfg->inter; dn.M_max = M; dn.m_count = Kstar;
   dn.W = w->w_down; dn.ldw = cfg->inter; dn.N = H;
   dn.out_f32 = x_out; dn.ldo = H;
+  dn.splits = L.split_down; dn.split_part = split;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_DOWN, EPI_RESID_F32, dn, stream));
   return DCUT_OK;
 }

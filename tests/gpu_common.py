@@ -10,6 +10,7 @@ from paper_2607_14647_amd import workload as wl
 
 LOGIT_RTOL = 2e-2      # max |l_gpu - l_ref| / max |l_ref| per row (bf16 path vs float64 oracle)
 ARGMAX_GAP = 1e-2      # argmax must match wherever the oracle's top-2 gap exceeds this
+ROUTER_GAP = 1e-2      # MoE rows compared where the oracle's k-th / (k+1)-th router-logit gap exceeds this
 X_RTOL = 2e-2          # residual rows and appended keys/values, same row-relative measure
 
 
@@ -32,6 +33,17 @@ def tiny_variants():
         "wide": dataclasses.replace(c1, cid=82, B=40, ctx=("uniform", 0, 40), budgets=(300,)),
         # block of one position (bonus only)
         "d0": dataclasses.replace(c1, cid=83, D=0, budgets=(4,)),
+        # a deep MLP: the down projection runs split-K
+        "deep": dataclasses.replace(c1, cid=84, B=8, budgets=(50,),
+                                    layer=dataclasses.replace(c1.layer, inter=2048)),
+        # routed MoE MLPs: 6 experts top-2; 128 experts top-8 with 8 query heads per kv head
+        "moe": dataclasses.replace(c1, cid=85, budgets=(30,),
+                                   layer=dataclasses.replace(c1.layer, inter=0, n_exp=6, top_k=2,
+                                                             exp_inter=40, rope_theta=1e6)),
+        "moe128": dataclasses.replace(c1, cid=86, B=16, budgets=(120,), ctx=("uniform", 300, 700),
+                                      layer=dataclasses.replace(c1.layer, n_q=8, n_kv=1, inter=0,
+                                                                n_exp=128, top_k=8, exp_inter=64,
+                                                                rope_theta=1e6)),
     }
 
 

@@ -16,8 +16,8 @@ from oracle import lm_head as olm
 from oracle import select as osel
 from paper_2607_14647_amd import lib as L
 from paper_2607_14647_amd import runner
-from tests.gpu_common import (ARGMAX_GAP, LOGIT_RTOL, X_RTOL, need_gpu, note, row_rel_err,
-                              tiny_variants, workload)
+from tests.gpu_common import (ARGMAX_GAP, LOGIT_RTOL, ROUTER_GAP, X_RTOL, need_gpu, note,
+                              row_rel_err, tiny_variants, workload)
 
 pytestmark = pytest.mark.gpu
 VARIANTS = tiny_variants()
@@ -60,7 +60,9 @@ def test_layer_parity(name, seed):
     assert int(vs.dev_err.item()) == 0
     assert np.array_equal(vs.host("cu"), sel["cu"])
     x = vs.x.cpu().numpy()[:K]
-    ex = row_rel_err(x, lay["x_out"])
+    # MoE: rows whose routing is a near-tie in the oracle are not compared
+    ok = lay["router_gap"] > ROUTER_GAP if "router_gap" in lay else np.ones(K, bool)
+    ex = row_rel_err(x[ok], lay["x_out"][ok])
     ly = cfg.layer
     # appended keys / values, and every other cache slot untouched
     kg = vs.kv["k"].cpu().numpy().view(np.uint16)
@@ -81,11 +83,11 @@ def test_layer_parity(name, seed):
             ek.append(np.abs(gv - lay["new_v"][t, g]).max() / np.abs(lay["new_v"][t, g]).max())
     assert np.array_equal(kg[~touched], kv["k"][~touched])
     assert np.array_equal(vg[~touched], kv["v"][~touched])
-    el = row_rel_err(logits[:K], lm["logits"])
+    el = row_rel_err(logits[:K][ok], lm["logits"][ok])
     am = vs.host("argmax")[:K]
-    sure = lm["gap"] > ARGMAX_GAP
+    sure = (lm["gap"] > ARGMAX_GAP) & ok
     note(f"  max rel err x={ex.max():.2e} kv={max(ek):.2e} logits={el.max():.2e}; "
-         f"argmax rows checked {sure.sum()}/{K}")
+         f"argmax rows checked {sure.sum()}/{K}; rows compared {ok.sum()}/{K}")
     assert ex.max() <= X_RTOL and max(ek) <= X_RTOL and el.max() <= LOGIT_RTOL
     assert np.array_equal(am[sure], lm["argmax"][sure])
     # max_logit is the logit at the argmax
@@ -123,7 +125,7 @@ def test_end_to_end_accept_with_forced_drafts(name):
     assert checked >= 2
 
 
-@pytest.mark.parametrize("name", ["cfg1", "long", "wide"])
+@pytest.mark.parametrize("name", ["cfg1", "long", "wide", "deep", "moe", "moe128"])
 def test_determinism_and_causality(name):
     """Same inputs -> identical bits; a kept row's outputs do not depend on the budget."""
     need_gpu()
