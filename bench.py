@@ -152,6 +152,9 @@ def main():
     ap.add_argument("--cost-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold", action="store_true", help="evict the MALL between timed steps")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="after the timed region, run a plain device-to-device copy of this many bytes "
+                         "three times (reference kernel for scaling HBM byte counters)")
     ap.add_argument("--state", default=None,
                     help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
                          "run of the same workload; written when missing, reused when present (a "
@@ -263,6 +266,13 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     L.profile_arm("NONE")
+    if args.copy_bytes > 0:
+        src = torch.ones(args.copy_bytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
     dom_us = 1000.0 * statistics.mean(a.elapsed_time(b) for a, b in kev)
