@@ -26,7 +26,8 @@ namespace dcut {
 
 namespace {
 
-constexpr int KT = 64;     // keys per tile
+constexpr int KT = 32;     // keys per tile
+constexpr int NSTAGE = 4;  // LDS ring stages: three tiles in flight while one is used
 
 // Cached length used for request i (clamped so bad device data stays in bounds)
 // and its number of chunks (at least one: the block keys).
@@ -40,17 +41,62 @@ __device__ __forceinline__ int n_chunks(int L, int chunk, int MC) {
   return nc > MC ? MC : nc;
 }
 
+typedef short short4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Barrier of the LDS ring: each wave has waited (s_waitcnt vmcnt) for its own
+// loads of the stage it reads next, so only the hardware barrier is needed; a
+// memory fence here would drain every stage still in flight.  The empty asm
+// statements keep the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Transposing LDS reads (ds_read_b64_tr_b16), four columns x two key halves per
+// call.  They are issued from one asm statement that also waits for them
+// (lgkmcnt(0)), so the compiler only ever sees completed results; it cannot
+// model these reads itself without also draining every LDS-DMA stage still in
+// flight (vmcnt(0)).  The ring protocol (vmcnt wait + barrier) orders them
+// after the DMA writes of the stage they read.
+__device__ __forceinline__ void lds_read_tr16_x8(short4v (&r)[8], const uint32_t (&ad)[8]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8\n\t"
+      "ds_read_b64_tr_b16 %1, %9\n\t"
+      "ds_read_b64_tr_b16 %2, %10\n\t"
+      "ds_read_b64_tr_b16 %3, %11\n\t"
+      "ds_read_b64_tr_b16 %4, %12\n\t"
+      "ds_read_b64_tr_b16 %5, %13\n\t"
+      "ds_read_b64_tr_b16 %6, %14\n\t"
+      "ds_read_b64_tr_b16 %7, %15\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+      : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "v"(ad[4]), "v"(ad[5]), "v"(ad[6]), "v"(ad[7])
+      : "memory");
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base, int bytes) {
+  const uintptr_t b = (uintptr_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const int n = __builtin_amdgcn_readfirstlane(bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(((uintptr_t)hi << 32) | lo), (short)0, n, 0x00020000);
+}
+
 template <int HD, int NW>
 __global__ void __launch_bounds__(NW * 64)
 k_attn(AttnArgs a) {
-  constexpr int LDKs = HD + 8;      // K tile row (bf16), 16-byte aligned rows
-  constexpr int LDV = KT + 2;       // V^T tile row (bf16): an odd number of words
-  constexpr int NS = HD / 32;       // k-steps of the QK product
-  constexpr int NT = HD / 16;       // 16-row tiles of O^T
-  constexpr int TOTCH = KT * (HD / 8);                 // 16-byte chunks per tile
-  constexpr int NCH = (TOTCH + NW * 64 - 1) / (NW * 64);  // per thread
-  __shared__ __align__(16) uint16_t Ks[KT * LDKs];
-  __shared__ __align__(16) uint16_t Vt[HD * LDV];
+  constexpr int ROWB = HD * 2;              // bytes per key row
+  constexpr int CPR = ROWB / 16;            // 16-byte chunks per key row (8 or 16)
+  constexpr int TILEB = KT * ROWB;          // bytes of one K (or V) tile
+  constexpr int STAGEB = 2 * TILEB;         // K tile then V tile
+  constexpr int RPI = 1024 / ROWB;          // key rows per 1 KB wave load
+  constexpr int LPK = (TILEB / 1024 + NW - 1) / NW;      // wave loads per stage for K (and for V)
+  constexpr int LPW = 2 * LPK;
+  constexpr int NS = HD / 32;               // k-steps of the QK product
+  constexpr int NT = HD / 16;               // 16-row tiles of O^T
+  __shared__ __align__(16) unsigned char ring[NSTAGE * STAGEB];
 
   const int MC = a.max_chunks;
   const int idx = blockIdx.x;
@@ -75,7 +121,8 @@ k_attn(AttnArgs a) {
 
   const int G = a.n_q / a.n_kv;
   const int R = G * d;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, grp4 = lane >> 4;
 
   // this lane's query row
@@ -108,69 +155,67 @@ k_attn(AttnArgs a) {
   float l_run = 0.0f;
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
 
+  // K and V of (request i, kv head g) as buffers: out-of-range keys read as zeros
   const size_t slab = (size_t)a.kv_base[i] + (size_t)g * cap * HD;
-  const uint16_t *kbase = a.kv_k + slab;
-  const uint16_t *vbase = a.kv_v + slab;
-
-  // chunk -> (key row, column): 8 lanes cover one key's 128 contiguous bytes
-  int ckr[NCH], cc8[NCH];
-  bool cok[NCH];
+  const int slab_bytes = cap * ROWB;
+  const __amdgpu_buffer_rsrc_t rK = uniform_rsrc(a.kv_k + slab, slab_bytes);
+  const __amdgpu_buffer_rsrc_t rV = uniform_rsrc(a.kv_v + slab, slab_bytes);
+  // Tile layout in LDS: key row r at r * ROWB; its 16-byte chunk c holds the
+  // row's global chunk c ^ (r % CPR), so 16 consecutive rows read at one column
+  // land in different banks.  A wave load fills RPI rows (1 KB): lane l writes
+  // row l / CPR, chunk l % CPR.
+  const int lrow = lane / CPR, lchk = lane % CPR;
+  auto issue = [&](int tile, int slot) {
+    const int p0 = kstart + tile * KT;
+    unsigned char *st = ring + slot * STAGEB;
 #pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    int ch = tid + j * NW * 64;
-    cok[j] = ch < TOTCH;
-    int blk = ch >> 6, l = ch & 63;
-    ckr[j] = (blk % (KT / 8)) * 8 + (l >> 3);
-    cc8[j] = (blk / (KT / 8)) * 64 + (l & 7) * 8;
-  }
-  uint4 rk[NCH], rv[NCH];
-  auto gload = [&](int p0) {
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      int p = p0 + ckr[j];
-      if (cok[j] && p < kend) {
-        rk[j] = *(const uint4 *)(kbase + (size_t)p * HD + cc8[j]);
-        rv[j] = *(const uint4 *)(vbase + (size_t)p * HD + cc8[j]);
-      } else {
-        rk[j] = make_uint4(0, 0, 0, 0);
-        rv[j] = make_uint4(0, 0, 0, 0);
-      }
+    for (int j = 0; j < LPK; ++j) {
+      const int q = wave + NW * j;                 // 1 KB block of the K (and V) tile
+      if (q >= TILEB / 1024) continue;
+      const int r = q * RPI + lrow;                // key row within the tile
+      const int p = p0 + r;
+      const unsigned off = p < kend ? (unsigned)(p * ROWB + 16 * (lchk ^ (r % CPR))) : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (lds_void *)(st + q * 1024), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (lds_void *)(st + TILEB + q * 1024), 16, off, 0, 0, 0);
     }
   };
 
   const int ntiles = (kend - kstart + KT - 1) / KT;
-  if (ntiles > 0) gload(kstart);
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < ntiles) issue(s, s);
+  constexpr int W0 = 0 | (7 << 4) | (15 << 8);
+  constexpr int W1 = (LPW & 15) | ((LPW >> 4) << 14) | (7 << 4) | (15 << 8);
+  constexpr int W2 = ((2 * LPW) & 15) | (((2 * LPW) >> 4) << 14) | (7 << 4) | (15 << 8);
   for (int tile = 0; tile < ntiles; ++tile) {
-    const int p0 = kstart + tile * KT;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      if (!cok[j]) continue;
-      *(uint4 *)(Ks + ckr[j] * LDKs + cc8[j]) = rk[j];
-      const uint16_t *ve = (const uint16_t *)&rv[j];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(cc8[j] + e) * LDV + ckr[j]] = ve[e];
-    }
-    __syncthreads();
-    if (tile + 1 < ntiles) gload(p0 + KT);
+    const int pending = min(NSTAGE - 2, ntiles - 1 - tile);
+    if (pending >= 2) __builtin_amdgcn_s_waitcnt(W2);
+    else if (pending == 1) __builtin_amdgcn_s_waitcnt(W1);
+    else __builtin_amdgcn_s_waitcnt(W0);
+    ring_barrier();
+    if (tile + NSTAGE - 1 < ntiles) issue(tile + NSTAGE - 1, (tile + NSTAGE - 1) % NSTAGE);
     if (!wave_active) continue;
+    const int p0 = kstart + tile * KT;
+    const unsigned char *Ks = ring + (tile % NSTAGE) * STAGEB;
+    const unsigned char *Vs = Ks + TILEB;
 
-    // S^T tiles: 4 blocks of 16 keys
-    floatx4 s4[4];
+    // S^T: KT/16 blocks of 16 keys; lane reads key row kb*16 + l16, global chunk 4s + grp4
+    floatx4 s4[KT / 16];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < KT / 16; ++kb) {
       s4[kb] = {0.f, 0.f, 0.f, 0.f};
-      const uint16_t *kp = Ks + (kb * 16 + l16) * LDKs + 8 * grp4;
+      const int r = kb * 16 + l16;
+      const unsigned char *kp = Ks + r * ROWB;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        bf16x8 kf = *(const bf16x8 *)(kp + 32 * s);
+        bf16x8 kf = *(const bf16x8 *)(kp + 16 * ((4 * s + grp4) ^ (r % CPR)));
         s4[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], s4[kb], 0, 0, 0);
       }
     }
     // mask + scale, tile max
     float tmax = -__builtin_inff();
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < KT / 16; ++kb)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         int p = p0 + kb * 16 + 4 * grp4 + j;
@@ -186,7 +231,7 @@ k_attn(AttnArgs a) {
     if (m_new != -__builtin_inff()) alpha = exp2f(m_run - m_new);
     float psum = 0.0f;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < KT / 16; ++kb)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         float v = s4[kb][j];
@@ -201,26 +246,43 @@ k_attn(AttnArgs a) {
 #pragma unroll
     for (int n = 0; n < NT; ++n) o[n] *= alpha;
 
-    // O^T += V^T P^T over two 32-key steps
+    // O^T += V^T P^T per 32-key step.  P^T slots of this lane: keys 4*grp4+j of the
+    // two 16-key blocks; the V^T fragment with the same keys comes from two
+    // transposing reads: source lane s of a 16-lane group reads key row
+    // k0 + s/4, columns 16n + 4(s%4)..+3, and lane d receives keys k0..k0+3 of
+    // column 16n + d.
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < KT / 32; ++ks) {
       bf16x8 pf;
       uint32_t *pw = (uint32_t *)&pf;
       pw[0] = pack_bf2(s4[2 * ks][0], s4[2 * ks][1]);
       pw[1] = pack_bf2(s4[2 * ks][2], s4[2 * ks][3]);
       pw[2] = pack_bf2(s4[2 * ks + 1][0], s4[2 * ks + 1][1]);
       pw[3] = pack_bf2(s4[2 * ks + 1][2], s4[2 * ks + 1][3]);
-      const int key_a = 32 * ks + 4 * grp4;          // keys key_a..+3 and key_a+16..+3
+      const int r0 = 32 * ks + 4 * grp4 + (l16 >> 2);      // source key row, first half
+      const int r1 = r0 + 16;
+      const int csub = 4 * (l16 & 3);                       // element offset within 16 columns
+      static_assert(NT % 4 == 0, "transposing reads come in groups of four columns");
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const uint32_t *vp = (const uint32_t *)(Vt + (n * 16 + l16) * LDV + key_a);
-        bf16x8 vf;
-        uint32_t *vw = (uint32_t *)&vf;
-        vw[0] = vp[0];
-        vw[1] = vp[1];
-        vw[2] = vp[8];
-        vw[3] = vp[9];
-        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[n], 0, 0, 0);
+      for (int n0 = 0; n0 < NT; n0 += 4) {
+        uint32_t ad[8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int col = 16 * (n0 + u) + csub;              // first of 4 columns read
+          const int gc = col >> 3, half = (col & 7) * 2;     // 16-byte chunk, byte offset in it
+          ad[2 * u] = (uint32_t)(uintptr_t)(Vs + r0 * ROWB + 16 * (gc ^ (r0 % CPR)) + half);
+          ad[2 * u + 1] = (uint32_t)(uintptr_t)(Vs + r1 * ROWB + 16 * (gc ^ (r1 % CPR)) + half);
+        }
+        short4v vr[8];
+        lds_read_tr16_x8(vr, ad);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          bf16x8 vf;
+          short4v *vw = (short4v *)&vf;
+          vw[0] = vr[2 * u];
+          vw[1] = vr[2 * u + 1];
+          o[n0 + u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[n0 + u], 0, 0, 0);
+        }
       }
     }
   }

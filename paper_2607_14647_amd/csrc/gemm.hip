@@ -1,7 +1,10 @@
 // bf16 NT GEMM on gfx950 MFMA with fused epilogues: C = A W^T, A [M][K], W [N][K].
 //
-// Block tile (2*WM*32) x (2*WN*32) x 64 with four waves in a 2 x 2 grid; every
-// wave owns WM x WN tiles of v_mfma_f32_32x32x16_bf16 (float32 accumulators).
+// Block tile (GM*WM*32) x (GN*WN*32) x 64 with GM x GN waves; every wave owns
+// WM x WN tiles of v_mfma_f32_32x32x16_bf16 (float32 accumulators).  Two
+// shapes: 128 x 128 (4 waves of 64 x 64) and, for GEMMs with many column
+// tiles, 256 x 256 (8 waves of 128 x 64), which halves the operand traffic
+// from L2 per flop.  The choice depends on the shape only, never on K*.
 // Operands go global -> registers -> LDS (double buffered, 16-byte padded rows),
 // with the next k-slice loaded while the current one is multiplied.  Residual
 // GEMMs with few output tiles split K over gridDim.y (a factor fixed by the
@@ -63,10 +66,11 @@ __device__ __forceinline__ int group_wrow(const GemmArgs &a, int grp) {
   }
 }
 
-template <int EPI, int WM, int WN>
-__global__ void __launch_bounds__(256)
+template <int EPI, int GM, int GN, int WM, int WN>
+__global__ void __launch_bounds__(GM * GN * 64)
 k_gemm(GemmArgs a) {
-  constexpr int TM = 64 * WM, TN = 64 * WN;
+  constexpr int NTH = GM * GN * 64;
+  constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
   extern __shared__ __align__(16) uint16_t lds[];   // [2][TM][LDK] (A) then [2][TN][LDK] (B)
 
   int M = *a.m_count;
@@ -89,9 +93,9 @@ k_gemm(GemmArgs a) {
   const int grp0 = nt * (TN / 32);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  constexpr int ACH = TM * TK / 8 / 256;    // 16-byte A chunks per thread
-  constexpr int BCH = TN * TK / 8 / 256;
+  const int wm = wave / GN, wn = wave % GN;
+  constexpr int ACH = TM * TK / 8 / NTH;    // 16-byte A chunks per thread
+  constexpr int BCH = TN * TK / 8 / NTH;
   uint16_t *As = lds;                        // [2][TM][LDK]
   uint16_t *Bs = lds + 2 * TM * LDK;         // [2][TN][LDK]
 
@@ -101,7 +105,7 @@ k_gemm(GemmArgs a) {
   int arow[ACH], acol[ACH];
 #pragma unroll
   for (int j = 0; j < ACH; ++j) {
-    int c = tid + 256 * j;
+    int c = tid + NTH * j;
     arow[j] = c >> 3;
     acol[j] = (c & 7) * 8;
     int gm = m0 + arow[j];
@@ -115,7 +119,7 @@ k_gemm(GemmArgs a) {
   int brow[BCH], bcol[BCH];
 #pragma unroll
   for (int j = 0; j < BCH; ++j) {
-    int c = tid + 256 * j;
+    int c = tid + NTH * j;
     brow[j] = c >> 3;
     bcol[j] = (c & 7) * 8;
     int wr = group_wrow<EPI>(a, grp0 + (brow[j] >> 5));
@@ -341,9 +345,10 @@ k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
   *o = acc;
 }
 
-template <int EPI, int WM, int WN>
+template <int EPI, int GM, int GN, int WM, int WN>
 int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
-  constexpr int TM = 64 * WM, TN = 64 * WN;
+  constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
+  constexpr int NTH = GM * GN * 64;
   int ncols = (EPI == EPI_SWIGLU) ? 2 * a.swiglu_inter : a.N;
   int nMT = a.m_tiles > 0 ? a.m_tiles : (a.M_max + TM - 1) / TM;
   int nNT = (EPI == EPI_SWIGLU) ? (a.swiglu_inter + TN / 2 - 1) / (TN / 2) : (ncols + TN - 1) / TN;
@@ -352,12 +357,12 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   if (splits > 1) {
     if ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32) || a.tiles || !a.split_part || a.N % 4 || a.ldo % 4)
       return DCUT_EINVAL;
-    DCUT_TRY(launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT, splits), dim3(256), shmem, s, a));
+    DCUT_TRY(launch(kid, k_gemm<EPI, GM, GN, WM, WN>, dim3(nMT * nNT, splits), dim3(NTH), shmem, s, a));
     return launch(DCUT_KERNEL_NONE, k_splitk_reduce, dim3((a.N + 1023) / 1024, a.M_max), dim3(256), 0, s,
                   (const float *)a.split_part, splits, a.M_max, a.N, a.m_count, a.out_f32, a.ldo,
                   EPI == EPI_RESID_F32 ? 1 : 0);
   }
-  return launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT), dim3(256), shmem, s, a);
+  return launch(kid, k_gemm<EPI, GM, GN, WM, WN>, dim3(nMT * nNT), dim3(NTH), shmem, s, a);
 }
 
 }  // namespace
@@ -372,14 +377,33 @@ int gemm_splits(int M_max, int N, int K) {
   return sp < 1 ? 1 : sp;
 }
 
+// 256 x 256 tiles when they still give at least one workgroup per CU, else 128 x 128.
+// Measured on MI355X: with one 8-wave workgroup per CU the 256 x 256 tile exposes
+// the global-load latency of every k-slice and runs slower than two 128 x 128
+// workgroups per CU, so the large tile is disabled until its loads are pipelined
+// deeper.
+constexpr bool kBigTiles = false;
+static bool use_big_tile(EpiKind epi, const GemmArgs &a) {
+  if (!kBigTiles || a.tiles || a.splits > 1) return false;
+  const int ncols = epi == EPI_SWIGLU ? 2 * a.swiglu_inter : a.N;
+  const long long tiles = (long long)((a.M_max + 255) / 256) * ((ncols + 255) / 256);
+  return tiles >= 256;
+}
+
+template <int EPI>
+static int launch_epi(int kid, const GemmArgs &a, hipStream_t s, bool big) {
+  return big ? launch_tile<EPI, 2, 4, 4, 2>(kid, a, s) : launch_tile<EPI, 2, 2, 2, 2>(kid, a, s);
+}
+
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {
+  const bool big = use_big_tile(epi, a);
   switch (epi) {
-    case EPI_STORE_BF16: return launch_tile<EPI_STORE_BF16, 2, 2>(kid, a, s);
-    case EPI_RESID_F32: return launch_tile<EPI_RESID_F32, 2, 2>(kid, a, s);
-    case EPI_SWIGLU: return launch_tile<EPI_SWIGLU, 2, 2>(kid, a, s);
-    case EPI_QKV_ROPE: return launch_tile<EPI_QKV_ROPE, 2, 2>(kid, a, s);
-    case EPI_ARGMAX: return launch_tile<EPI_ARGMAX, 2, 2>(kid, a, s);
-    case EPI_STORE_F32: return launch_tile<EPI_STORE_F32, 2, 2>(kid, a, s);
+    case EPI_STORE_BF16: return launch_epi<EPI_STORE_BF16>(kid, a, s, big);
+    case EPI_RESID_F32: return launch_epi<EPI_RESID_F32>(kid, a, s, big);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(kid, a, s, big);
+    case EPI_QKV_ROPE: return launch_epi<EPI_QKV_ROPE>(kid, a, s, big);
+    case EPI_ARGMAX: return launch_epi<EPI_ARGMAX>(kid, a, s, big);
+    case EPI_STORE_F32: return launch_epi<EPI_STORE_F32>(kid, a, s, big);
   }
   return DCUT_EINVAL;
 }
