@@ -1,12 +1,13 @@
 // bf16 NT GEMM on gfx950 MFMA with fused epilogues: C = A W^T, A [M][K], W [N][K].
 //
-// Block tile (GM*WM*32) x (GN*WN*32) x 64 with GM x GN waves; every wave owns
-// WM x WN tiles of v_mfma_f32_32x32x16_bf16 (float32 accumulators).  Two
-// shapes: 128 x 128 (4 waves of 64 x 64) and, for GEMMs with many column
-// tiles, 256 x 256 (8 waves of 128 x 64), which halves the operand traffic
-// from L2 per flop.  The choice depends on the shape only, never on K*.
-// Operands go global -> registers -> LDS (double buffered, 16-byte padded rows),
-// with the next k-slice loaded while the current one is multiplied.  Residual
+// Block tile (2*WM*32) x (2*WN*32) x 64 with four waves in a 2 x 2 grid; every
+// wave owns WM x WN tiles of v_mfma_f32_32x32x16_bf16 (float32 accumulators).
+// Operands stream from memory straight into a double-buffered LDS ring (buffer
+// loads with the LDS destination, XOR-swizzled 16-byte chunks, hardware zeros
+// for rows and k beyond the operands), so the next k-slice is in flight while
+// the current one is multiplied and no registers stage it.  64 KB of LDS per
+// workgroup keeps two workgroups resident per CU; deeper rings and larger tiles
+// measured slower on MI355X (fewer resident workgroups).  Residual
 // GEMMs with few output tiles split K over gridDim.y (a factor fixed by the
 // shape); k_splitk_reduce then adds the partial tiles in split order.
 //
@@ -22,6 +23,7 @@
 // Tile order is XCD-major: consecutive workgroups of one XCD (the hardware
 // deals workgroups round-robin over 8 XCDs) walk the row tiles of the same
 // column tiles, so the W slice they share stays in that XCD's L2.
+
 #include "dcut_internal.h"
 
 namespace dcut {
@@ -29,7 +31,7 @@ namespace dcut {
 namespace {
 
 constexpr int TK = 64;
-constexpr int LDK = TK + 8;   // 144-byte LDS rows
+constexpr int NSTAGE = 2;     // LDS stages: one k-slice in flight while the other is multiplied
 
 __device__ __forceinline__ uint32_t orderable(float v) {
   uint32_t u = __float_as_uint(v);
@@ -38,6 +40,16 @@ __device__ __forceinline__ uint32_t orderable(float v) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// Workgroup barrier for the LDS ring: each wave has already waited (s_waitcnt
+// vmcnt) for its own loads of the stage it is about to read, so no memory fence
+// (which would drain every stage still in flight) is needed, only the hardware
+// barrier; the empty asm statements keep the compiler from moving LDS accesses
+// across it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // W row feeding logical tile column group `grp` (global, 32 columns each), plus
 // the first output column of that group; returns -1 when the group is past N.
@@ -66,12 +78,12 @@ __device__ __forceinline__ int group_wrow(const GemmArgs &a, int grp) {
   }
 }
 
-template <int EPI, int GM, int GN, int WM, int WN>
-__global__ void __launch_bounds__(GM * GN * 64)
+template <int EPI, int WM, int WN>
+__global__ void __launch_bounds__(256)
 k_gemm(GemmArgs a) {
-  constexpr int NTH = GM * GN * 64;
+  constexpr int GM = 2, GN = 2, NWV = GM * GN;
   constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
-  extern __shared__ __align__(16) uint16_t lds[];   // [2][TM][LDK] (A) then [2][TN][LDK] (B)
+  extern __shared__ __align__(16) uint16_t lds[];   // [NSTAGE][TM*TK (A) + TN*TK (B)]
 
   int M = *a.m_count;
   const int nMT = a.m_tiles > 0 ? a.m_tiles : (a.M_max + TM - 1) / TM;
@@ -94,67 +106,67 @@ k_gemm(GemmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / GN, wn = wave % GN;
-  constexpr int ACH = TM * TK / 8 / NTH;    // 16-byte A chunks per thread
-  constexpr int BCH = TN * TK / 8 / NTH;
-  uint16_t *As = lds;                        // [2][TM][LDK]
-  uint16_t *Bs = lds + 2 * TM * LDK;         // [2][TN][LDK]
 
-  // per-thread load descriptors
-  const uint16_t *aptr[ACH];
-  bool aval[ACH];
-  int arow[ACH], acol[ACH];
+  // Operand loads go straight from memory to LDS (buffer_load ... lds): each
+  // wave instruction fills one 1 KB block = 8 rows x 64 k (128 B per row).
+  // Block q holds rows 8q..8q+7; in row r the 16-byte chunk c holds global k
+  // chunk c ^ (r & 7), so the MFMA fragment reads of 32 consecutive rows spread
+  // over all LDS banks.  Out-of-range rows and k chunks get an offset past the
+  // buffer end and read as zeros.
+  const int a_rows_ext = a.a_extent > 0 ? a.a_extent : a.M_max;
+  const long long a_bytes = (long long)a_rows_ext * a.lda * 2;
+  const int w_rows_ext = (EPI == EPI_SWIGLU) ? 2 * a.swiglu_inter : a.N;
+  const long long w_bytes = (long long)w_rows_ext * a.ldw * 2;
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)a.A, (short)0, (int)(a_bytes < 0x7fffffffLL ? a_bytes : 0x7fffffffLL), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)Wb, (short)0, (int)(w_bytes < 0x7fffffffLL ? w_bytes : 0x7fffffffLL), 0x00020000);
+  constexpr unsigned OOB = 0x80000000u;
+  constexpr int CPR = TK / 8, RPI = 64 / CPR;   // 16-byte chunks per row, rows per 1 KB wave load
+  constexpr int AJ = TM / (NWV * RPI), BJ = TN / (NWV * RPI);     // load instructions per wave per stage
+  const int lr = lane / CPR, lc = lane % CPR;
+  unsigned aoff[AJ], boff[BJ];
+  int akc[AJ], bkc[BJ];
 #pragma unroll
-  for (int j = 0; j < ACH; ++j) {
-    int c = tid + NTH * j;
-    arow[j] = c >> 3;
-    acol[j] = (c & 7) * 8;
-    int gm = m0 + arow[j];
-    aval[j] = gm < M;
-    int src = aval[j] ? gm : 0;
-    if (a.a_rows && aval[j]) src = a.a_rows[gm];
-    aptr[j] = a.A + (size_t)src * a.lda + acol[j];
+  for (int j = 0; j < AJ; ++j) {
+    const int r = RPI * (wave + NWV * j) + lr;
+    akc[j] = 8 * (lc ^ (r % CPR));                 // first k of the chunk this lane fetches
+    const int gm = m0 + r;
+    unsigned off = OOB;
+    if (gm < M) {
+      const int src = a.a_rows ? a.a_rows[gm] : gm;
+      off = (unsigned)(((long long)src * a.lda + akc[j]) * 2);
+    }
+    aoff[j] = off;
   }
-  const uint16_t *bptr[BCH];
-  bool bval[BCH];
-  int brow[BCH], bcol[BCH];
 #pragma unroll
-  for (int j = 0; j < BCH; ++j) {
-    int c = tid + NTH * j;
-    brow[j] = c >> 3;
-    bcol[j] = (c & 7) * 8;
-    int wr = group_wrow<EPI>(a, grp0 + (brow[j] >> 5));
-    int r = wr + (brow[j] & 31);
+  for (int j = 0; j < BJ; ++j) {
+    const int r = RPI * (wave + NWV * j) + lr;
+    bkc[j] = 8 * (lc ^ (r % CPR));
+    const int grp = grp0 + (r >> 5);
+    const int wr = group_wrow<EPI>(a, grp);
     bool ok = wr >= 0;
-    if (EPI == EPI_SWIGLU) ok = ok && ((((grp0 + (brow[j] >> 5)) >> 1) * 32 + (brow[j] & 31)) < a.swiglu_inter);
-    else ok = ok && r < a.N;
-    bval[j] = ok;
-    bptr[j] = Wb + (size_t)(ok ? r : 0) * a.ldw + bcol[j];
+    if (EPI == EPI_SWIGLU) ok = ok && ((grp >> 1) * 32 + (r & 31)) < a.swiglu_inter;
+    else ok = ok && wr + (r & 31) < a.N;
+    boff[j] = ok ? (unsigned)(((long long)(wr + (r & 31)) * a.ldw + bkc[j]) * 2) : OOB;
   }
-
-  // the next k-slice is loaded into registers while the current one is multiplied
-  uint4 ra[ACH], rb[BCH];
-  auto gload = [&](int kt) {
+  constexpr int STAGE = (TM + TN) * TK;            // bf16 elements per stage
+  auto issue = [&](int kt, int slot) {
     const int k0 = kt * TK;
+    uint16_t *sa = lds + slot * STAGE;
+    uint16_t *sb = sa + TM * TK;
 #pragma unroll
-    for (int j = 0; j < ACH; ++j) {
-      const bool ok = aval[j] && k0 + acol[j] < a.K;
-      const uint4 v = *(const uint4 *)(aptr[j] + (ok ? k0 : 0));
-      ra[j] = ok ? v : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < AJ; ++j) {
+      const unsigned off = (aoff[j] != OOB && k0 + akc[j] < a.K) ? aoff[j] + (unsigned)k0 * 2 : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (__attribute__((address_space(3))) void *)(sa + (wave + NWV * j) * 512),
+                                               16, off, 0, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < BCH; ++j) {
-      const bool ok = bval[j] && k0 + bcol[j] < a.K;
-      const uint4 v = *(const uint4 *)(bptr[j] + (ok ? k0 : 0));
-      rb[j] = ok ? v : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < BJ; ++j) {
+      const unsigned off = (boff[j] != OOB && k0 + bkc[j] < a.K) ? boff[j] + (unsigned)k0 * 2 : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (__attribute__((address_space(3))) void *)(sb + (wave + NWV * j) * 512),
+                                               16, off, 0, 0, 0);
     }
-  };
-  auto lstore = [&](int buf) {
-    uint16_t *as = As + buf * TM * LDK;
-    uint16_t *bs = Bs + buf * TN * LDK;
-#pragma unroll
-    for (int j = 0; j < ACH; ++j) *(uint4 *)(as + arow[j] * LDK + acol[j]) = ra[j];
-#pragma unroll
-    for (int j = 0; j < BCH; ++j) *(uint4 *)(bs + brow[j] * LDK + bcol[j]) = rb[j];
   };
 
   floatx16 acc[WM][WN];
@@ -165,37 +177,57 @@ k_gemm(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int l32 = lane & 31, khalf = (lane >> 5) * 8;
+  const int l32 = lane & 31, kh = lane >> 5;
+  // fragment read offsets within a stage (row r: block r>>3, row r&7, chunk swizzled by r&7)
+  int afrag[WM], bfrag[WN], arx[WM], brx[WN];
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+    const int r = wm * WM * 32 + i * 32 + l32;
+    afrag[i] = r * TK;
+    arx[i] = r % CPR;
+  }
+#pragma unroll
+  for (int j = 0; j < WN; ++j) {
+    const int r = wn * WN * 32 + j * 32 + l32;
+    bfrag[j] = TM * TK + r * TK;
+    brx[j] = r % CPR;
+  }
+
   // this workgroup's k range (split-K over gridDim.y, fixed by the shape)
   const int nk_all = (a.K + TK - 1) / TK;
   const int per_split = (nk_all + (int)gridDim.y - 1) / (int)gridDim.y;
   const int kt0 = (int)blockIdx.y * per_split;
   const int nk = max(0, min(nk_all, kt0 + per_split) - kt0);
-  if (nk > 0) {
-    gload(kt0);
-    lstore(0);
-    __syncthreads();
-  }
+  // s_waitcnt immediates waiting for all but 0, 1 or 2 stages of AJ+BJ loads
+  constexpr int LPS = AJ + BJ;
+  constexpr int W0 = 0 | (7 << 4) | (15 << 8);
+  constexpr int W1 = (LPS & 15) | ((LPS >> 4) << 14) | (7 << 4) | (15 << 8);
+  constexpr int W2 = ((2 * LPS) & 15) | (((2 * LPS) >> 4) << 14) | (7 << 4) | (15 << 8);
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < nk) issue(kt0 + s, s);
   for (int it = 0; it < nk; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nk) gload(kt0 + it + 1);
-    const uint16_t *as = As + buf * TM * LDK + (wm * WM * 32 + l32) * LDK + khalf;
-    const uint16_t *bs = Bs + buf * TN * LDK + (wn * WN * 32 + l32) * LDK + khalf;
+    const int pending = min(NSTAGE - 2, nk - 1 - it);
+    if (pending >= 2) __builtin_amdgcn_s_waitcnt(W2);
+    else if (pending == 1) __builtin_amdgcn_s_waitcnt(W1);
+    else __builtin_amdgcn_s_waitcnt(W0);
+    ring_barrier();
+    if (it + NSTAGE - 1 < nk) issue(kt0 + it + NSTAGE - 1, (it + NSTAGE - 1) % NSTAGE);
+    const uint16_t *st = lds + (it % NSTAGE) * STAGE;
 #pragma unroll
     for (int ks = 0; ks < TK / 16; ++ks) {
+      const int kc = 2 * ks + kh;
       bf16x8 af[WM], bf[WN];
 #pragma unroll
-      for (int i = 0; i < WM; ++i) af[i] = *(const bf16x8 *)(as + i * 32 * LDK + ks * 16);
+      for (int i = 0; i < WM; ++i) af[i] = *(const bf16x8 *)(st + afrag[i] + 8 * (kc ^ arx[i]));
 #pragma unroll
-      for (int j = 0; j < WN; ++j) bf[j] = *(const bf16x8 *)(bs + j * 32 * LDK + ks * 16);
+      for (int j = 0; j < WN; ++j) bf[j] = *(const bf16x8 *)(st + bfrag[j] + 8 * (kc ^ brx[j]));
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < WN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    if (it + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
   }
 
   if (gridDim.y > 1) {
@@ -345,24 +377,23 @@ k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
   *o = acc;
 }
 
-template <int EPI, int GM, int GN, int WM, int WN>
+template <int EPI, int WM, int WN>
 int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
-  constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
-  constexpr int NTH = GM * GN * 64;
+  constexpr int TM = 2 * WM * 32, TN = 2 * WN * 32;
   int ncols = (EPI == EPI_SWIGLU) ? 2 * a.swiglu_inter : a.N;
   int nMT = a.m_tiles > 0 ? a.m_tiles : (a.M_max + TM - 1) / TM;
   int nNT = (EPI == EPI_SWIGLU) ? (a.swiglu_inter + TN / 2 - 1) / (TN / 2) : (ncols + TN - 1) / TN;
-  size_t shmem = (size_t)2 * (TM + TN) * LDK * sizeof(uint16_t);
+  size_t shmem = (size_t)NSTAGE * (TM + TN) * TK * sizeof(uint16_t);
   const int splits = a.splits > 1 ? a.splits : 1;
   if (splits > 1) {
     if ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32) || a.tiles || !a.split_part || a.N % 4 || a.ldo % 4)
       return DCUT_EINVAL;
-    DCUT_TRY(launch(kid, k_gemm<EPI, GM, GN, WM, WN>, dim3(nMT * nNT, splits), dim3(NTH), shmem, s, a));
+    DCUT_TRY(launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT, splits), dim3(256), shmem, s, a));
     return launch(DCUT_KERNEL_NONE, k_splitk_reduce, dim3((a.N + 1023) / 1024, a.M_max), dim3(256), 0, s,
                   (const float *)a.split_part, splits, a.M_max, a.N, a.m_count, a.out_f32, a.ldo,
                   EPI == EPI_RESID_F32 ? 1 : 0);
   }
-  return launch(kid, k_gemm<EPI, GM, GN, WM, WN>, dim3(nMT * nNT), dim3(NTH), shmem, s, a);
+  return launch(kid, k_gemm<EPI, WM, WN>, dim3(nMT * nNT), dim3(256), shmem, s, a);
 }
 
 }  // namespace
@@ -377,33 +408,14 @@ int gemm_splits(int M_max, int N, int K) {
   return sp < 1 ? 1 : sp;
 }
 
-// 256 x 256 tiles when they still give at least one workgroup per CU, else 128 x 128.
-// Measured on MI355X: with one 8-wave workgroup per CU the 256 x 256 tile exposes
-// the global-load latency of every k-slice and runs slower than two 128 x 128
-// workgroups per CU, so the large tile is disabled until its loads are pipelined
-// deeper.
-constexpr bool kBigTiles = false;
-static bool use_big_tile(EpiKind epi, const GemmArgs &a) {
-  if (!kBigTiles || a.tiles || a.splits > 1) return false;
-  const int ncols = epi == EPI_SWIGLU ? 2 * a.swiglu_inter : a.N;
-  const long long tiles = (long long)((a.M_max + 255) / 256) * ((ncols + 255) / 256);
-  return tiles >= 256;
-}
-
-template <int EPI>
-static int launch_epi(int kid, const GemmArgs &a, hipStream_t s, bool big) {
-  return big ? launch_tile<EPI, 2, 4, 4, 2>(kid, a, s) : launch_tile<EPI, 2, 2, 2, 2>(kid, a, s);
-}
-
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {
-  const bool big = use_big_tile(epi, a);
   switch (epi) {
-    case EPI_STORE_BF16: return launch_epi<EPI_STORE_BF16>(kid, a, s, big);
-    case EPI_RESID_F32: return launch_epi<EPI_RESID_F32>(kid, a, s, big);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(kid, a, s, big);
-    case EPI_QKV_ROPE: return launch_epi<EPI_QKV_ROPE>(kid, a, s, big);
-    case EPI_ARGMAX: return launch_epi<EPI_ARGMAX>(kid, a, s, big);
-    case EPI_STORE_F32: return launch_epi<EPI_STORE_F32>(kid, a, s, big);
+    case EPI_STORE_BF16: return launch_tile<EPI_STORE_BF16, 2, 2>(kid, a, s);
+    case EPI_RESID_F32: return launch_tile<EPI_RESID_F32, 2, 2>(kid, a, s);
+    case EPI_SWIGLU: return launch_tile<EPI_SWIGLU, 2, 2>(kid, a, s);
+    case EPI_QKV_ROPE: return launch_tile<EPI_QKV_ROPE, 2, 2>(kid, a, s);
+    case EPI_ARGMAX: return launch_tile<EPI_ARGMAX, 2, 2>(kid, a, s);
+    case EPI_STORE_F32: return launch_tile<EPI_STORE_F32, 2, 2>(kid, a, s);
   }
   return DCUT_EINVAL;
 }
