@@ -347,10 +347,10 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
 
 template <int HD>
 int launch_hd(const AttnArgs &a, int rows_max, const int32_t *packed_req, int waves, hipStream_t s) {
+  // at least 8 waves: the extra waves share the tile loads, which measured
+  // faster than 4 waves per workgroup (16 waves measured slower)
   const dim3 grid(a.B * a.n_kv * a.max_chunks);
-  if (waves <= 4) {
-    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 4>, grid, dim3(256), 0, s, a));
-  } else if (waves <= 8) {
+  if (waves <= 8) {
     DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 8>, grid, dim3(512), 0, s, a));
   } else {
     DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 16>, grid, dim3(1024), 0, s, a));

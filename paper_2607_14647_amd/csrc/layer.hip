@@ -14,9 +14,14 @@
 
 namespace dcut {
 
-// Split-KV chunk length (cache keys per attention work item).  A function of
-// the shapes only, never of the kept rows.
-constexpr int ATTN_CHUNK = 512;
+// Split-KV chunk length (cache keys per attention work item): 1024 keys when the
+// batch still gives at least 2048 work items, else 512.  A function of the
+// shapes only (B, n_kv, max_ctx), never of the kept rows, so a row's partial
+// sums never depend on the budget.
+static int attn_chunk(const dcut_layer_cfg *c, int B) {
+  const long long items = (long long)B * c->n_kv * ((c->max_ctx + 1023) / 1024);
+  return items >= 2048 ? 1024 : 512;
+}
 
 struct LayerWs {
   size_t h, q, attn, rope, part, mid, split, moe, total;
@@ -46,7 +51,8 @@ static LayerWs layer_ws(const dcut_layer_cfg *c, int B, int D) {
   LayerWs w;
   const size_t M = (size_t)B * (D + 1);
   const size_t qd = (size_t)c->n_q * c->head_dim;
-  const int mc = (c->max_ctx + ATTN_CHUNK - 1) / ATTN_CHUNK;
+  const int chunk = attn_chunk(c, B);
+  const int mc = (c->max_ctx + chunk - 1) / chunk;
   size_t off = 0;
   w.h = off; off = align256(off + M * c->hidden * 2);
   w.q = off; off = align256(off + M * qd * 2);
@@ -120,7 +126,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   AttnArgs at = {};
   at.q = q; at.kv_k = kv->k; at.kv_v = kv->v; at.kv_base = kv->base; at.kv_cap = kv->cap;
   at.cu = cu; at.ctx_len = ctx_len; at.B = B; at.D = D; at.n_q = nq; at.n_kv = nkv; at.head_dim = hd;
-  at.chunk = ATTN_CHUNK; at.max_chunks = (cfg->max_ctx + ATTN_CHUNK - 1) / ATTN_CHUNK;
+  at.chunk = attn_chunk(cfg, B); at.max_chunks = (cfg->max_ctx + at.chunk - 1) / at.chunk;
   at.part = part; at.out = att; at.dev_err = dev_err;
   const int waves = ((nq / nkv) * (D + 1) + 15) / 16;
   DCUT_TRY(attention_launch(at, M, packed_req, waves, stream));
