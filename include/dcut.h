@@ -165,7 +165,9 @@ int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *w, int B, i
  *
  * f = RMSNorm(x) * final_norm (eps), logits = f W_lm^T accumulated in float32,
  * argmax = the lowest vocabulary id among the row maxima (greedy target
- * decoding, Sec. 4.1).  Logits are never materialised unless `logits` is given.
+ * decoding, Sec. 4.1).  Logits are never materialised unless `logits` is given;
+ * the workspace holds the normalised rows and up to one partial maximum per row
+ * and 64 columns of the vocabulary.
  *
  *   H, V     hidden size and vocabulary
  *   cu       dev [B+1] from dcut_select (K* = cu[B])
@@ -173,7 +175,8 @@ int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *w, int B, i
  *   w_lm     dev [V][H] bf16
  *   argmax   dev [B(D+1)] int32 out;   max_logit dev [B(D+1)] float32 out (nullable)
  *   logits   dev [B(D+1)][V] float32 out (nullable, for checking only)
- *   ws       dev scratch of dcut_workspace_bytes(2, cfg with hidden = H, B, D) bytes
+ *   ws       dev scratch of dcut_workspace_bytes(2, cfg with hidden = H and vocab = V,
+ *            B, D) bytes, 256-byte aligned
  * Supported: H multiple of 8.
  */
 int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,

@@ -4,7 +4,7 @@
 
 namespace dcut {
 size_t layer_ws_bytes(const dcut_layer_cfg *c, int B, int D);
-size_t lmhead_ws_bytes(int H, int B, int D);
+size_t lmhead_ws_bytes(int H, int V, int B, int D);
 
 ProfileHook &profile_hook() {
   static thread_local ProfileHook h = {DCUT_KERNEL_NONE, nullptr, nullptr};
@@ -31,8 +31,8 @@ extern "C" size_t dcut_workspace_bytes(int which, const dcut_layer_cfg *cfg, int
     case 0: return 0;
     case 1: return layer_ws_bytes(cfg, B, D);
     case 2:
-      if (!cfg || cfg->hidden <= 0 || cfg->hidden % 8) return (size_t)-1;
-      return lmhead_ws_bytes(cfg->hidden, B, D);
+      if (!cfg || cfg->hidden <= 0 || cfg->hidden % 8 || cfg->vocab <= 0) return (size_t)-1;
+      return lmhead_ws_bytes(cfg->hidden, cfg->vocab, B, D);
     case 3: return 0;
   }
   return (size_t)-1;

@@ -100,7 +100,8 @@ struct GemmArgs {
   const int32_t *kv_cap;
   int n_q, n_kv, head_dim;
   // EPI_ARGMAX
-  unsigned long long *amax_keys;  // [M_max]
+  unsigned long long *amax_keys;  // [M_max][amax_slots]: per-row maxima of column ranges
+  int amax_slots;                 // row stride of amax_keys, at least gemm_argmax_slots()
   float *logits;                  // optional [M][N] float32
   long long ld_logits;
   // split-K (EPI_RESID_F32 / EPI_STORE_F32): partial tiles [splits][M_max][N] float32
@@ -118,6 +119,8 @@ struct GemmArgs {
 };
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s);
+// number of per-row partial argmax keys EPI_ARGMAX writes for this shape (at most 2 * ceil(N / 128))
+int gemm_argmax_slots(const GemmArgs &a);
 // split-K factor for a residual GEMM of this shape (a function of M_max, never of K*)
 int gemm_splits(int M_max, int N, int K);
 

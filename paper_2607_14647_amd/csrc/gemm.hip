@@ -392,6 +392,9 @@ k_gemm(GemmArgs a) {
           }
         }
     } else if (EPI == EPI_ARGMAX) {
+      // one key per row and wave column range (WN * 32 columns): plain stores,
+      // merged by a later pass
+      const int slot = nt * GN + wn;
 #pragma unroll
       for (int i = 0; i < WM; ++i) {
 #pragma unroll
@@ -413,7 +416,7 @@ k_gemm(GemmArgs a) {
             unsigned long long o = __shfl_xor(best, off, 64);
             best = o > best ? o : best;
           }
-          if (l32 == 0 && gm < Mlim && best) atomicMax(a.amax_keys + gm, best);
+          if (l32 == 0 && gm < Mlim) a.amax_keys[(size_t)gm * a.amax_slots + slot] = best;
         }
       }
     }
@@ -459,6 +462,7 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   const int nMT = a.tiles ? a.m_tiles : (a.M_max + T::TM - 1) / T::TM;
   const int nNT = EPI == EPI_SWIGLU ? (a.swiglu_inter + T::TN / 2 - 1) / (T::TN / 2) : (a.N + T::TN - 1) / T::TN;
   const int splits = a.splits > 1 ? a.splits : 1;
+  if (EPI == EPI_ARGMAX && (!a.amax_keys || a.amax_slots < nNT * T::GN)) return DCUT_EINVAL;
   if (splits > 1 && ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32) || a.tiles || !a.split_part || a.N % 4 ||
                      a.ldo % 4))
     return DCUT_EINVAL;
@@ -498,6 +502,12 @@ int gemm_splits(int M_max, int N, int K) {
   if (sp > cap) sp = cap;
   if (sp > 16) sp = 16;
   return sp < 1 ? 1 : sp;
+}
+
+int gemm_argmax_slots(const GemmArgs &a) {
+  const bool big = !a.tiles && a.splits <= 1 &&
+                   (long long)((a.M_max + Big::TM - 1) / Big::TM) * ((a.N + Big::TN - 1) / Big::TN) >= cu_count();
+  return big ? (a.N + Big::TN - 1) / Big::TN * Big::GN : (a.N + Small::TN - 1) / Small::TN * Small::GN;
 }
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {

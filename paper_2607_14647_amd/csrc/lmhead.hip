@@ -1,26 +1,47 @@
 // dcut_lm_head_argmax: final RMSNorm, LM-head GEMM with a fused row argmax.
 //
-// The GEMM epilogue reduces each row's slice of the vocabulary to one 64-bit
-// key (order-preserving logit bits << 32 | ~column) and merges it with an
-// atomic max, so the full logits are never written and the merge is
-// independent of workgroup order; the lowest column wins exact ties.
+// The GEMM epilogue reduces each row's column ranges of the vocabulary (64 or
+// 128 columns, by tile shape) to one 64-bit key each (order-preserving logit
+// bits << 32 | ~column) and stores them; a second pass takes the maximum key
+// of every row.  The full logits are
+// never written, no atomics contend on a row, the result does not depend on
+// workgroup order, and the lowest column wins exact ties.
 #include "dcut_internal.h"
 
 namespace dcut {
 
-size_t lmhead_ws_bytes(int H, int B, int D) {
+size_t lmhead_ws_bytes(int H, int V, int B, int D) {
   const size_t M = (size_t)B * (D + 1);
-  return align256(M * H * 2) + align256(M * sizeof(unsigned long long));
+  const size_t slots = 2 * (((size_t)V + 127) / 128);   // row stride of the partial keys
+  return align256(M * H * 2) + align256(M * slots * sizeof(unsigned long long));
 }
 
 namespace {
 
+// One workgroup per row: the maximum of the row's partial keys, decoded.
 __global__ void __launch_bounds__(256)
-k_argmax_final(const unsigned long long *__restrict__ keys, const int32_t *__restrict__ m_count,
-               int M_max, int32_t *__restrict__ argmax, float *__restrict__ max_logit) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
+k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int stride,
+               const int32_t *__restrict__ m_count, int M_max, int32_t *__restrict__ argmax,
+               float *__restrict__ max_logit) {
+  __shared__ unsigned long long s_max[4];
+  const int t = blockIdx.x;
   if (t >= M_max || t >= *m_count) return;
-  unsigned long long k = keys[t];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const unsigned long long *row = keys + (size_t)t * stride;
+  unsigned long long k = 0ull;
+  for (int s = tid; s < slots; s += 256) {
+    const unsigned long long v = row[s];
+    k = v > k ? v : k;
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned long long o = __shfl_xor(k, off, 64);
+    k = o > k ? o : k;
+  }
+  if (lane == 0) s_max[tid >> 6] = k;
+  __syncthreads();
+  if (tid != 0) return;
+  for (int w = 1; w < 4; ++w) k = s_max[w] > k ? s_max[w] : k;
   argmax[t] = (int32_t)(0xffffffffu - (uint32_t)(k & 0xffffffffu));
   if (max_logit) {
     uint32_t u = (uint32_t)(k >> 32);
@@ -40,19 +61,21 @@ extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu
                                    size_t ws_bytes, hipStream_t stream) {
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
   if (!cu || !x || !final_norm || !w_lm || !argmax || !(eps >= 0.0f)) return DCUT_EINVAL;
-  const size_t need = lmhead_ws_bytes(H, B, D);
+  const size_t need = lmhead_ws_bytes(H, V, B, D);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
   uint16_t *f = (uint16_t *)ws;
   unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)M * H * 2));
   const int32_t *Kstar = cu + B;
+  const int slots = 2 * ((V + 127) / 128);   // row stride; the GEMM writes gemm_argmax_slots() of them
   DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x, nullptr, nullptr, 0, final_norm, eps, H, M, Kstar,
-                          nullptr, f, nullptr, 0, 0.0f, nullptr, keys, nullptr, stream));
+                          nullptr, f, nullptr, 0, 0.0f, nullptr, nullptr, nullptr, stream));
   GemmArgs g = {};
   g.A = f; g.lda = H; g.K = H; g.M_max = M; g.m_count = Kstar;
   g.W = w_lm; g.ldw = H; g.N = V;
-  g.amax_keys = keys; g.logits = logits; g.ld_logits = V;
+  g.amax_keys = keys; g.amax_slots = slots; g.logits = logits; g.ld_logits = V;
+  const int used = gemm_argmax_slots(g);
   DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, EPI_ARGMAX, g, stream));
-  return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3((M + 255) / 256), dim3(256), 0, stream,
-                (const unsigned long long *)keys, Kstar, M, argmax, max_logit);
+  return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3(M), dim3(256), 0, stream,
+                (const unsigned long long *)keys, used, slots, Kstar, M, argmax, max_logit);
 }

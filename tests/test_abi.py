@@ -62,7 +62,8 @@ def test_workspace_sizes():
     assert L.workspace_bytes(3, None, 64, 15) == 0
     ws1 = L.workspace_bytes(1, cfg, 64, 15)
     assert 0 < ws1 < (1 << 31) and ws1 % 256 == 0
-    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 1024 * 8
+    # normalised rows plus up to one key per row and 64 columns of the vocabulary
+    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 1024 * 2 * ((cfg.vocab + 127) // 128) * 8
     assert L.workspace_bytes(1, cfg, 0, 15) == 2 ** 64 - 1
     bad = L.LayerCfg(4096, 32, 7, 128, 14336, 0, 0, 0, 128256, 4112, 1e-5, 5e5)
     assert L.workspace_bytes(1, bad, 64, 15) == 2 ** 64 - 1
