@@ -392,33 +392,60 @@ k_gemm(GemmArgs a) {
           }
         }
     } else if (EPI == EPI_ARGMAX) {
-      // one key per row and wave column range (WN * 32 columns): plain stores,
-      // merged by a later pass
+      // One key per row and wave column range (WN * 32 columns), stored and
+      // merged by a later pass.  Each lane first takes the maximum over its WN
+      // columns; the 32 column keys of a row then go through LDS (idle after the
+      // k loop) and one lane per row takes their maximum, which avoids a chain
+      // of dependent cross-lane shuffles per row.
+      static_assert(WM * 32 == 64, "one lane per row of the wave");
+      constexpr int KS = 33;                        // keys per LDS row, one pad
+      static_assert((size_t)NWV * 64 * KS * 8 <= T::LDS, "key transpose fits the rings");
+      unsigned long long *kl = (unsigned long long *)lds + (size_t)wave * 64 * KS;
       const int slot = nt * GN + wn;
+      const int col0 = (grp0 + wn * WN) * 32 + l32;   // this lane's column in group j: col0 + 32 j
+      if (a.logits) {
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int gm = rbase + i * 32 + 8 * (r >> 2) + (r & 3);
+            if (gm < Mlim)
+#pragma unroll
+              for (int j = 0; j < WN; ++j)
+                if (col0 + 32 * j < a.N) a.logits[(size_t)gm * a.ld_logits + col0 + 32 * j] = acc[i][j][r];
+          }
+      }
+      // branch-free per-lane maximum over the WN columns (increasing with j):
+      // a strictly larger order key replaces, so the lowest column wins ties
 #pragma unroll
       for (int i = 0; i < WM; ++i) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          int gm = rbase + i * 32 + 8 * (r >> 2) + (r & 3);
-          unsigned long long best = 0ull;
+          uint32_t bo = 0u, bc = 0xffffffffu;
 #pragma unroll
           for (int j = 0; j < WN; ++j) {
-            int col = (grp0 + wn * WN + j) * 32 + l32;
-            if (col < a.N) {
-              float v = acc[i][j][r];
-              unsigned long long key = ((unsigned long long)orderable(v) << 32) | (0xffffffffu - (uint32_t)col);
-              best = key > best ? key : best;
-              if (a.logits && gm < Mlim) a.logits[(size_t)gm * a.ld_logits + col] = v;
-            }
+            const uint32_t c = (uint32_t)(col0 + 32 * j);
+            const uint32_t o = c < (uint32_t)a.N ? orderable(acc[i][j][r]) : 0u;
+            const bool up = o > bo;
+            bo = up ? o : bo;
+            bc = up ? c : bc;
           }
-#pragma unroll
-          for (int off = 1; off < 32; off <<= 1) {
-            unsigned long long o = __shfl_xor(best, off, 64);
-            best = o > best ? o : best;
-          }
-          if (l32 == 0 && gm < Mlim) a.amax_keys[(size_t)gm * a.amax_slots + slot] = best;
+          const int q = i * 32 + 8 * (r >> 2) + 4 * kh + (r & 3);   // row within the wave
+          kl[q * KS + l32] = ((unsigned long long)bo << 32) | (0xffffffffu - bc);
         }
       }
+      __builtin_amdgcn_wave_barrier();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      unsigned long long best = 0ull;
+#pragma unroll 8
+      for (int c = 0; c < 32; ++c) {
+        const unsigned long long v = kl[lane * KS + c];
+        best = v > best ? v : best;
+      }
+      const int gm = m0 + wm * WM * 32 + lane;
+      if (gm < Mlim) a.amax_keys[(size_t)gm * a.amax_slots + slot] = best;
+      // the next task's prologue refills the LDS this pass used
+      ring_barrier();
     }
   }
 }
