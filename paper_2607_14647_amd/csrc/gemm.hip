@@ -116,6 +116,34 @@ __device__ __forceinline__ int n_col_tiles(const GemmArgs &a, int TN) {
   return EPI == EPI_SWIGLU ? (a.swiglu_inter + TN / 2 - 1) / (TN / 2) : (a.N + TN - 1) / TN;
 }
 
+// QKV epilogue for one RoPE pair of one row: x1, x2 = projections at head
+// dimensions j and j + hd/2.  q and k heads are rotated; q goes to out_bf16, k
+// and v to the request's cache slot (slots outside the cache are skipped; the
+// norm kernel reports them).
+__device__ __forceinline__ void qkv_emit(const GemmArgs &a, int gm, int head, int j, float x1, float x2) {
+  const int hd = a.head_dim, half = hd >> 1;
+  float o1 = x1, o2 = x2;
+  if (head < a.n_q + a.n_kv) {
+    const float2 cs = a.rope_cs[(size_t)gm * half + j];
+    o1 = x1 * cs.x - x2 * cs.y;
+    o2 = x2 * cs.x + x1 * cs.y;
+  }
+  if (head < a.n_q) {
+    uint16_t *q = a.out_bf16 + (size_t)gm * a.ldo + head * hd;
+    q[j] = f2bf(o1);
+    q[j + half] = f2bf(o2);
+  } else {
+    const int req = a.packed_req[gm];
+    const int slot = a.packed_pos[gm];
+    const int cap = a.kv_cap[req];
+    if (slot < 0 || slot >= cap) return;
+    const int g = (head < a.n_q + a.n_kv) ? head - a.n_q : head - a.n_q - a.n_kv;
+    uint16_t *dst = (head < a.n_q + a.n_kv ? a.kv_k : a.kv_v) + a.kv_base[req] + ((size_t)g * cap + slot) * hd;
+    dst[j] = f2bf(o1);
+    dst[j + half] = f2bf(o2);
+  }
+}
+
 template <int EPI, class T>
 __global__ void __launch_bounds__(T::THREADS)
 k_gemm(GemmArgs a) {
@@ -294,15 +322,17 @@ k_gemm(GemmArgs a) {
     ring_barrier();
 
     if (splits > 1) {
-      // split-K partial tile; k_splitk_reduce applies the epilogue in split order
+      // split-K partial tile at the true output columns; the reduce pass adds
+      // the splits in order and applies the epilogue
       float *part = a.split_part + (size_t)sp * a.M_max * a.N;
       const int rb_ = m0 + wm * WM * 32 + 4 * (lane >> 5);
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-          int col = (grp0 + wn * WN + j) * 32 + l32;
-          if (col >= a.N) continue;
+          const int wr = group_wrow<EPI>(a, grp0 + wn * WN + j);
+          const int col = wr + l32;
+          if (wr < 0 || col >= a.N) continue;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             int gm = rb_ + i * 32 + 8 * (r >> 2) + (r & 3);
@@ -353,7 +383,7 @@ k_gemm(GemmArgs a) {
           }
         }
     } else if (EPI == EPI_QKV_ROPE) {
-      const int hd = a.head_dim, half = hd >> 1, gph = hd / 32;
+      const int hd = a.head_dim, gph = hd / 32;
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -366,29 +396,7 @@ k_gemm(GemmArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             int gm = rbase + i * 32 + 8 * (r >> 2) + (r & 3);
-            if (gm >= Mlim) continue;
-            float x1 = acc[i][2 * p][r], x2 = acc[i][2 * p + 1][r];
-            float o1 = x1, o2 = x2;
-            if (head < a.n_q + a.n_kv) {
-              float2 cs = a.rope_cs[(size_t)gm * half + j];
-              o1 = x1 * cs.x - x2 * cs.y;
-              o2 = x2 * cs.x + x1 * cs.y;
-            }
-            if (head < a.n_q) {
-              uint16_t *q = a.out_bf16 + (size_t)gm * a.ldo + head * hd;
-              q[j] = f2bf(o1);
-              q[j + half] = f2bf(o2);
-            } else {
-              int req = a.packed_req[gm];
-              int slot = a.packed_pos[gm];
-              int cap = a.kv_cap[req];
-              if (slot < 0 || slot >= cap) continue;      // reported by the norm kernel
-              int g = (head < a.n_q + a.n_kv) ? head - a.n_q : head - a.n_q - a.n_kv;
-              uint16_t *dst = (head < a.n_q + a.n_kv ? a.kv_k : a.kv_v) + a.kv_base[req] +
-                              ((size_t)g * cap + slot) * hd;
-              dst[j] = f2bf(o1);
-              dst[j + half] = f2bf(o2);
-            }
+            if (gm < Mlim) qkv_emit(a, gm, head, j, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
           }
         }
     } else if (EPI == EPI_ARGMAX) {
@@ -471,6 +479,27 @@ k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
   *o = acc;
 }
 
+// QKV split-K epilogue: one thread per (row, head, RoPE pair); the partials of
+// dimensions j and j + hd/2 added in split order, then the QKV epilogue.
+__global__ void __launch_bounds__(256)
+k_qkv_reduce(GemmArgs a) {
+  const int m = blockIdx.y;
+  if (m >= *a.m_count) return;
+  const int half = a.head_dim >> 1, nh = a.n_q + 2 * a.n_kv;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= nh * half) return;
+  const int head = idx / half, j = idx - head * half;
+  const size_t c1 = (size_t)head * a.head_dim + j, c2 = c1 + half;
+  const float *p = a.split_part + (size_t)m * a.N;
+  float x1 = p[c1], x2 = p[c2];
+  for (int s = 1; s < a.splits; ++s) {
+    const float *q = a.split_part + ((size_t)s * a.M_max + m) * a.N;
+    x1 += q[c1];
+    x2 += q[c2];
+  }
+  qkv_emit(a, m, head, j, x1, x2);
+}
+
 int cu_count() {
   static int n = 0;
   if (n == 0) {
@@ -490,8 +519,8 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   const int nNT = EPI == EPI_SWIGLU ? (a.swiglu_inter + T::TN / 2 - 1) / (T::TN / 2) : (a.N + T::TN - 1) / T::TN;
   const int splits = a.splits > 1 ? a.splits : 1;
   if (EPI == EPI_ARGMAX && (!a.amax_keys || a.amax_slots < nNT * T::GN)) return DCUT_EINVAL;
-  if (splits > 1 && ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32) || a.tiles || !a.split_part || a.N % 4 ||
-                     a.ldo % 4))
+  if (splits > 1 && ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32 && EPI != EPI_QKV_ROPE) || a.tiles ||
+                     !a.split_part || a.N % 4 || (EPI != EPI_QKV_ROPE && a.ldo % 4)))
     return DCUT_EINVAL;
   // persistent grid: one wave of workgroups, a multiple of 8 (one share per XCD)
   const long long tasks = (long long)nMT * nNT * splits;
@@ -500,6 +529,10 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   g = (g + 7) / 8 * 8;
   if (g < 8) g = 8;
   DCUT_TRY(launch(kid, k_gemm<EPI, T>, dim3((unsigned)g), dim3(T::THREADS), T::LDS, s, a));
+  if (splits > 1 && EPI == EPI_QKV_ROPE) {
+    const int pairs = (a.n_q + 2 * a.n_kv) * (a.head_dim / 2);
+    return launch(DCUT_KERNEL_NONE, k_qkv_reduce, dim3((pairs + 255) / 256, a.M_max), dim3(256), 0, s, a);
+  }
   if (splits > 1)
     return launch(DCUT_KERNEL_NONE, k_splitk_reduce, dim3((a.N + 1023) / 1024, a.M_max), dim3(256), 0, s,
                   (const float *)a.split_part, splits, a.M_max, a.N, a.m_count, a.out_f32, a.ldo,

@@ -25,7 +25,7 @@ static int attn_chunk(const dcut_layer_cfg *c, int B) {
 
 struct LayerWs {
   size_t h, q, attn, rope, part, mid, split, moe, total;
-  int split_o, split_down;
+  int split_qkv, split_o, split_down;
 };
 
 static bool layer_cfg_ok(const dcut_layer_cfg *c, int B, int D) {
@@ -60,10 +60,16 @@ static LayerWs layer_ws(const dcut_layer_cfg *c, int B, int D) {
   w.rope = off; off = align256(off + M * (c->head_dim / 2) * sizeof(float2));
   w.part = off; off = align256(off + M * c->n_q * (size_t)mc * (c->head_dim + 2) * sizeof(float));
   w.mid = off; off = align256(off + (c->n_exp == 0 ? M * (size_t)c->inter * 2 : 0));
+  const size_t nqkv = (size_t)(c->n_q + 2 * c->n_kv) * c->head_dim;
+  w.split_qkv = gemm_splits((int)M, (int)nqkv, c->hidden);
   w.split_o = gemm_splits((int)M, c->hidden, (int)qd);
   w.split_down = c->n_exp == 0 ? gemm_splits((int)M, c->hidden, c->inter) : 1;
-  const int sp = w.split_o > w.split_down ? w.split_o : w.split_down;
-  w.split = off; off = align256(off + (sp > 1 ? (size_t)sp * M * c->hidden * sizeof(float) : 0));
+  size_t split_floats = 0;   // per row, the largest of the three split-K partial sets
+  if (w.split_qkv > 1) split_floats = (size_t)w.split_qkv * nqkv;
+  if (w.split_o > 1 && (size_t)w.split_o * c->hidden > split_floats) split_floats = (size_t)w.split_o * c->hidden;
+  if (w.split_down > 1 && (size_t)w.split_down * c->hidden > split_floats)
+    split_floats = (size_t)w.split_down * c->hidden;
+  w.split = off; off = align256(off + M * split_floats * sizeof(float));
   w.moe = off;
   if (c->n_exp > 0) off = align256(off + moe_ws_bytes((int)M, c->hidden, c->n_exp, c->top_k, c->exp_inter));
   w.total = off;
@@ -121,6 +127,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   g.packed_pos = packed_pos; g.packed_req = packed_req; g.ctx_len = ctx_len; g.rope_cs = rope;
   g.kv_k = kv->k; g.kv_v = kv->v; g.kv_base = kv->base; g.kv_cap = kv->cap;
   g.n_q = nq; g.n_kv = nkv; g.head_dim = hd;
+  g.splits = L.split_qkv; g.split_part = split;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_QKV, EPI_QKV_ROPE, g, stream));
   // 3. attention
   AttnArgs at = {};

@@ -44,6 +44,11 @@ def tiny_variants():
                                       layer=dataclasses.replace(c1.layer, n_q=8, n_kv=1, inter=0,
                                                                 n_exp=128, top_k=8, exp_inter=64,
                                                                 rope_theta=1e6)),
+        # head_dim 128, split-K QKV (RoPE in the reduce pass), O and down projections, and a
+        # vocabulary wide enough for the 256 x 256 LM-head tiles
+        "split": dataclasses.replace(c1, cid=87, budgets=(40,),
+                                     layer=dataclasses.replace(c1.layer, hidden=1024, n_q=8, n_kv=2,
+                                                               head_dim=128, inter=2048, vocab=65536)),
     }
 
 
