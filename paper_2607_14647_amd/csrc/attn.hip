@@ -98,12 +98,15 @@ k_attn(AttnArgs a) {
   constexpr int NT = HD / 16;               // 16-row tiles of O^T
   __shared__ __align__(16) unsigned char ring[NSTAGE * STAGEB];
 
+  // Chunk index slowest: the work items that exist for every request (the first
+  // chunks) come first, so workgroups of chunks a request does not have are
+  // dispatched last and exit without holding a slot among live ones.
   const int MC = a.max_chunks;
   const int idx = blockIdx.x;
-  const int c = idx % MC;
-  const int g = (idx / MC) % a.n_kv;
-  const int i = idx / (MC * a.n_kv);
-  if (i >= a.B) return;
+  const int c = idx / (a.B * a.n_kv);
+  const int g = idx % a.n_kv;
+  const int i = (idx / a.n_kv) % a.B;
+  if (c >= MC) return;
   const int t0 = a.cu[i];
   const int d = a.cu[i + 1] - t0;
   const int L0 = a.ctx_len[i];
