@@ -53,6 +53,7 @@ struct Tile {
   static constexpr int PER_CU = LDS > 81920 ? 1 : 2;
 };
 using Big = Tile<4, 2, 2, 4>;
+using Mid = Tile<2, 4, 2, 2>;     // 128 x 256, eight waves in a 2 x 4 grid, 128 KB
 using Small = Tile<2, 2, 2, 2>;
 
 __device__ __forceinline__ uint32_t orderable(float v) {
@@ -145,8 +146,7 @@ __device__ __forceinline__ void qkv_emit(const GemmArgs &a, int gm, int head, in
 }
 
 template <int EPI, class T>
-__global__ void __launch_bounds__(T::THREADS)
-k_gemm(GemmArgs a) {
+__device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
   constexpr int GM = T::GM, GN = T::GN, WM = T::WM, WN = T::WN, NWV = T::NWV;
   constexpr int TM = T::TM, TN = T::TN, NA = T::NA, NB = T::NB;
   constexpr int AJ = TM / (NWV * RPI), BJ = TN / (NWV * RPI);   // load instructions per wave per stage
@@ -399,16 +399,15 @@ k_gemm(GemmArgs a) {
             if (gm < Mlim) qkv_emit(a, gm, head, j, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
           }
         }
-    } else if (EPI == EPI_ARGMAX) {
+    } else if constexpr (EPI == EPI_ARGMAX) {
       // One key per row and wave column range (WN * 32 columns), stored and
       // merged by a later pass.  Each lane first takes the maximum over its WN
-      // columns; the 32 column keys of a row then go through LDS (idle after the
-      // k loop) and one lane per row takes their maximum, which avoids a chain
-      // of dependent cross-lane shuffles per row.
-      static_assert(WM * 32 == 64, "one lane per row of the wave");
+      // columns; the 32 column keys of each of 32 rows then go through LDS (idle
+      // after the k loop) and one lane per row takes their maximum, which avoids
+      // a chain of dependent cross-lane shuffles per row.
       constexpr int KS = 33;                        // keys per LDS row, one pad
-      static_assert((size_t)NWV * 64 * KS * 8 <= T::LDS, "key transpose fits the rings");
-      unsigned long long *kl = (unsigned long long *)lds + (size_t)wave * 64 * KS;
+      static_assert((size_t)NWV * 32 * KS * 8 <= T::LDS, "key transpose fits the rings");
+      unsigned long long *kl = (unsigned long long *)lds + (size_t)wave * 32 * KS;
       const int slot = nt * GN + wn;
       const int col0 = (grp0 + wn * WN) * 32 + l32;   // this lane's column in group j: col0 + 32 j
       if (a.logits) {
@@ -423,10 +422,10 @@ k_gemm(GemmArgs a) {
                 if (col0 + 32 * j < a.N) a.logits[(size_t)gm * a.ld_logits + col0 + 32 * j] = acc[i][j][r];
           }
       }
-      // branch-free per-lane maximum over the WN columns (increasing with j):
-      // a strictly larger order key replaces, so the lowest column wins ties
 #pragma unroll
       for (int i = 0; i < WM; ++i) {
+        // branch-free per-lane maximum over the WN columns (increasing with j):
+        // a strictly larger order key replaces, so the lowest column wins ties
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           uint32_t bo = 0u, bc = 0xffffffffu;
@@ -438,24 +437,49 @@ k_gemm(GemmArgs a) {
             bo = up ? o : bo;
             bc = up ? c : bc;
           }
-          const int q = i * 32 + 8 * (r >> 2) + 4 * kh + (r & 3);   // row within the wave
+          const int q = 8 * (r >> 2) + 4 * kh + (r & 3);   // row within these 32
           kl[q * KS + l32] = ((unsigned long long)bo << 32) | (0xffffffffu - bc);
         }
-      }
-      __builtin_amdgcn_wave_barrier();
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      unsigned long long best = 0ull;
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if (lane < 32) {
+          unsigned long long best = 0ull;
 #pragma unroll 8
-      for (int c = 0; c < 32; ++c) {
-        const unsigned long long v = kl[lane * KS + c];
-        best = v > best ? v : best;
+          for (int c = 0; c < 32; ++c) {
+            const unsigned long long v = kl[lane * KS + c];
+            best = v > best ? v : best;
+          }
+          const int gm = m0 + wm * WM * 32 + i * 32 + lane;
+          if (gm < Mlim) a.amax_keys[(size_t)gm * a.amax_slots + slot] = best;
+        }
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       }
-      const int gm = m0 + wm * WM * 32 + lane;
-      if (gm < Mlim) a.amax_keys[(size_t)gm * a.amax_slots + slot] = best;
       // the next task's prologue refills the LDS this pass used
       ring_barrier();
     }
   }
+}
+
+template <int EPI, class T>
+__global__ void __launch_bounds__(T::THREADS)
+k_gemm(GemmArgs a) {
+  gemm_tasks<EPI, T>(a);
+}
+
+// Dense GEMM whose tile shape follows the live row count M (read on the device):
+// 128 x 256 tiles when 256 x 256 tiles would leave a quarter or more of the
+// persistent workgroups without a task, else 256 x 256.  Every element is the
+// same sequence of MFMA k-steps in both shapes, so the choice never changes a
+// result bit.
+template <int EPI>
+__global__ void __launch_bounds__(Big::THREADS)
+k_gemm_dual(GemmArgs a) {
+  static_assert(Mid::THREADS == Big::THREADS && Mid::LDS <= Big::LDS, "one launch shape for both tiles");
+  const int M = *a.m_count;
+  const long long big_tasks = (long long)((M + Big::TM - 1) / Big::TM) * n_col_tiles<EPI>(a, Big::TN);
+  if (4 * big_tasks < 3LL * gridDim.x) gemm_tasks<EPI, Mid>(a);
+  else gemm_tasks<EPI, Big>(a);
 }
 
 // out[m][n] (+)= sum over splits of part[s][m][n], in split order (rows m < K*).
@@ -540,16 +564,23 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   return DCUT_OK;
 }
 
-// Big tiles for dense GEMMs with at least one Big tile per CU at M_max rows;
-// Small tiles for the others, for grouped (MoE row tiles of 128) and for
-// split-K GEMMs.  The choice depends on the shape only.
+// Big tiles for dense GEMMs with at least one Big tile per CU at M_max rows
+// (the SwiGLU GEMM picks Big or Mid on the device from the live rows); Small
+// tiles for the others, for grouped (MoE row tiles of 128) and for split-K
+// GEMMs.
 template <int EPI>
 int launch_epi(int kid, const GemmArgs &a, hipStream_t s) {
   if (a.tiles || a.splits > 1) return launch_tile<EPI, Small>(kid, a, s);
   const long long big_tasks = (long long)((a.M_max + Big::TM - 1) / Big::TM) *
       (EPI == EPI_SWIGLU ? (a.swiglu_inter + Big::TN / 2 - 1) / (Big::TN / 2) : (a.N + Big::TN - 1) / Big::TN);
   if (big_tasks < cu_count()) return launch_tile<EPI, Small>(kid, a, s);
-  return launch_tile<EPI, Big>(kid, a, s);
+  if constexpr (EPI == EPI_SWIGLU) {
+    // tile shape chosen on the device from the live row count (one workgroup per CU)
+    const int g = (cu_count() + 7) / 8 * 8;
+    return launch(kid, k_gemm_dual<EPI>, dim3((unsigned)g), dim3(Big::THREADS), Big::LDS, s, a);
+  } else {
+    return launch_tile<EPI, Big>(kid, a, s);
+  }
 }
 
 }  // namespace
