@@ -1,7 +1,7 @@
 // Greedy target-only acceptance (Sec. 3.2: sequential acceptance; App. A).
 //
-// One workgroup; one thread per request walks its kept block until the first
-// draft that differs from the target's greedy token at the previous row.
+// One workgroup.  Every (request, depth) pair is compared at once; the first
+// mismatch of each request (an LDS minimum) gives its accepted length.
 #include "dcut_internal.h"
 #include "scan.h"
 
@@ -13,17 +13,29 @@ k_accept(int B, int D, const int32_t *__restrict__ draft, const int32_t *__restr
          int32_t *__restrict__ accept_len, int32_t *__restrict__ next_tok,
          int32_t *__restrict__ total, int32_t *__restrict__ ctx_len_inout) {
   __shared__ int s_wave[17];
+  __shared__ int s_n[DCUT_MAX_BATCH], s_base[DCUT_MAX_BATCH], s_first[DCUT_MAX_BATCH];
   const int D1 = D + 1;
   const int rows = B * D1;
-  int local = 0;
   for (int i = threadIdx.x; i < B; i += blockDim.x) {
     int n = keep_len[i] - 1;
     n = n < 0 ? 0 : (n > D ? D : n);
     int base = cu[i];
     base = base < 0 ? 0 : (base > rows - 1 - n ? rows - 1 - n : base);   // stay in bounds
-    const int32_t *z = draft + (size_t)i * D1;
-    int a = 0;
-    while (a < n && z[a + 1] == argmax[base + a]) ++a;
+    s_n[i] = n;
+    s_base[i] = base;
+    s_first[i] = n;                     // no mismatch among the n checked drafts
+  }
+  __syncthreads();
+  // draft j+1 of request i is checked against the greedy token of row base + j
+  for (int idx = threadIdx.x; idx < B * D; idx += blockDim.x) {
+    const int i = idx / D, j = idx - i * D;
+    if (j < s_n[i] && draft[(size_t)i * D1 + j + 1] != argmax[s_base[i] + j]) atomicMin(&s_first[i], j);
+  }
+  __syncthreads();
+  int local = 0;
+  for (int i = threadIdx.x; i < B; i += blockDim.x) {
+    const int a = s_first[i];
+    const int base = s_base[i];
     accept_len[i] = a;
     next_tok[i] = argmax[base + a];
     local += a + 1;

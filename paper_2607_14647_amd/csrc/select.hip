@@ -51,14 +51,17 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   int NP = 64;
   while (NP < N) NP <<= 1;
   unsigned long long *keys = smem;          // [NP]
+  float *s_conf = (float *)(smem + NP + blockDim.x);   // [B * D], staged once (coalesced)
   if (tid == 0) s_err = 0;
+  for (int j = tid; j < B * D; j += blockDim.x) s_conf[j] = conf[j];
+  __syncthreads();
 
   // 1. scores and keys, one thread per request, sequential in depth
   for (int i = tid; i < B; i += blockDim.x) {
     float s = 1.0f;
     keys[i * D1] = rank_key(s, 0, i);
     for (int k = 1; k <= D; ++k) {
-      float c = conf[(size_t)i * D + (k - 1)];
+      float c = s_conf[i * D + (k - 1)];
       if (conf_bad(c)) {
         s_err = 1;
         c = 0.0f;
@@ -132,7 +135,7 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
     float s = 1.0f;
     int n = 1;                        // the bonus key (s = 1, k = 0) always ranks first in its request
     for (int k = 1; k <= D; ++k) {
-      float c = conf[(size_t)i * D + (k - 1)];
+      float c = s_conf[i * D + (k - 1)];
       if (conf_bad(c)) c = 0.0f;
       s = s * c;
       if (rank_key(s, k, i) >= tau) n = k + 1;
@@ -214,7 +217,7 @@ extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft
   }
   int N = B * (D + 1), NP = 64;
   while (NP < N) NP <<= 1;
-  size_t shmem = (size_t)(NP + 1024) * sizeof(unsigned long long);
+  size_t shmem = (size_t)(NP + 1024) * sizeof(unsigned long long) + (size_t)B * D * sizeof(float);
   DCUT_TRY(launch(DCUT_KERNEL_SELECT, k_select, dim3(1), dim3(1024), shmem, stream, p, conf,
                   keep_len, choice, (unsigned long long *)benefit, dev_err));
   DCUT_TRY(launch(DCUT_KERNEL_PACK, k_pack, dim3(1), dim3(1024), 0, stream, B, D,
