@@ -73,17 +73,43 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   for (int j = N + tid; j < NP; j += blockDim.x) keys[j] = 0ull;   // sorts last
 
   // 2. bitonic sort, descending
-  for (int size = 2; size <= NP; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      __syncthreads();
-      for (int t = tid; t < (NP >> 1); t += blockDim.x) {
-        int lo = 2 * t - (t & (stride - 1));
-        int hi = lo + stride;
-        unsigned long long a = keys[lo], b = keys[hi];
-        bool desc = (lo & size) == 0;
-        if (desc ? (a < b) : (a > b)) {
-          keys[lo] = b;
-          keys[hi] = a;
+  if (NP <= (int)blockDim.x) {
+    // one key per thread: compare-exchange partners closer than a wave apart
+    // swap through cross-lane shuffles (no barrier), farther ones through LDS
+    __syncthreads();
+    const bool act = tid < NP;               // whole waves (NP is a multiple of 64)
+    unsigned long long x = act ? keys[tid] : 0ull;
+    for (int size = 2; size <= NP; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        unsigned long long y;
+        if (stride >= 64) {
+          __syncthreads();
+          if (act) keys[tid] = x;
+          __syncthreads();
+          y = act ? keys[tid ^ stride] : 0ull;
+        } else {
+          y = __shfl_xor(x, stride, 64);
+        }
+        // the lower index of a pair keeps the larger key in a descending run
+        const bool take_max = ((tid & stride) == 0) == ((tid & size) == 0);
+        x = take_max ? (x > y ? x : y) : (x < y ? x : y);
+      }
+    }
+    __syncthreads();
+    if (act) keys[tid] = x;
+  } else {
+    for (int size = 2; size <= NP; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        __syncthreads();
+        for (int t = tid; t < (NP >> 1); t += blockDim.x) {
+          int lo = 2 * t - (t & (stride - 1));
+          int hi = lo + stride;
+          unsigned long long a = keys[lo], b = keys[hi];
+          bool desc = (lo & size) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            keys[lo] = b;
+            keys[hi] = a;
+          }
         }
       }
     }
