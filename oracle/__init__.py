@@ -18,8 +18,10 @@ Modules
              Eq. dcut-objective; Alg. 1; App. C packing)
   layer   -- one decoder layer over the packed rows (dense SwiGLU or MoE)
   lm_head -- final norm, logits and greedy argmax
+  sampling -- temperature-T target sampling (Gumbel-max over Philox4x32-10
+             uniforms), the paper's temperature-1 regime
   accept  -- greedy target-only longest-prefix acceptance (Sec. 3.2, App. A)
   drafts  -- forced-match draft construction for tests and benchmarks
 """
 from .errors import DcutArgError, DcutDataError, DERR_CONF, DERR_TOKEN, DERR_CAPACITY  # noqa: F401
-from . import select, layer, lm_head, accept  # noqa: F401
+from . import select, layer, lm_head, accept, sampling  # noqa: F401
