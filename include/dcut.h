@@ -9,6 +9,11 @@
  *   dcut_lm_head_argmax  final norm, LM head and greedy argmax of every kept row
  *   dcut_accept          greedy longest-prefix acceptance       (Sec. 3.2; App. A)
  *
+ * and, for temperature-T target sampling (Sec. 4, sampling regimes), the
+ * drop-in replacement of the third call:
+ *
+ *   dcut_lm_head_sample  final norm, LM head and a Gumbel-max draw per kept row
+ *
  * Conventions shared by every call
  *   - All pointers marked "dev" are device pointers on the current HIP device;
  *     "host" pointers are read during the call only.  The caller owns every
@@ -183,6 +188,35 @@ int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const flo
                         const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
                         int32_t *argmax, float *max_logit, float *logits,
                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * dcut_lm_head_sample -- target token of every kept row drawn at temperature T.
+ *
+ * Temperature-T target sampling with target-only verification (Sec. 4,
+ * robustness across sampling regimes; App. A, correctness): the token of row t
+ * is argmax_c (logits[t][c] / T + G(t, c)), the lowest id among equal scores,
+ * which is distributed as softmax(logits[t] / T).  G = -ln(-ln u) is standard
+ * Gumbel noise; u comes from Philox4x32-10 (Salmon et al., SC 2011) keyed by
+ * `seed` (low 32 bits first):
+ *   counter = (32 * (c >> 7) + (c & 31), packed_pos[t], packed_req[t], 0),
+ *   u = (word (c >> 5) & 3 of the output + 0.5) / 2^32,
+ * so the draw of a (request, position) never depends on what else the batch
+ * keeps.  Logits, scaling and noise are float32.  dcut_accept then takes
+ * `token` in place of the greedy argmax.
+ *
+ *   packed_req, packed_pos  dev [B(D+1)] from dcut_select
+ *   temperature             > 0 and finite
+ *   token     dev [B(D+1)] int32 out;   max_score dev [B(D+1)] float32 out (nullable):
+ *             the winning logits / T + G
+ *   other arguments and the workspace as for dcut_lm_head_argmax
+ * Errors: DCUT_EINVAL for a null request/position array or a temperature that
+ * is not positive and finite, otherwise as dcut_lm_head_argmax.
+ */
+int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu, const int32_t *packed_req,
+                        const int32_t *packed_pos, const float *x, const dcut_bf16 *final_norm,
+                        float eps, const dcut_bf16 *w_lm, float temperature, uint64_t seed,
+                        int32_t *token, float *max_score, void *ws, size_t ws_bytes,
+                        hipStream_t stream);
 
 /*
  * dcut_accept -- greedy target-only acceptance (Sec. 3.2, App. A).

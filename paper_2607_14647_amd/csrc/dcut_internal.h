@@ -78,8 +78,9 @@ enum EpiKind {
   EPI_RESID_F32 = 1,    // out_f32[m][n] += acc   (residual add, in place)
   EPI_SWIGLU = 2,       // W rows interleaved by tile: out_bf16[m][j] = SiLU(gate) * up
   EPI_QKV_ROPE = 3,     // RoPE + scatter q to out_bf16, k/v into the cache
-  EPI_ARGMAX = 4,       // per-row max/argmax merged with 64-bit atomics
-  EPI_STORE_F32 = 5     // out_f32[m][n] = acc
+  EPI_ARGMAX = 4,       // per-row max/argmax: one u64 key per row and wave column range
+  EPI_STORE_F32 = 5,    // out_f32[m][n] = acc
+  EPI_SAMPLE = 6        // as EPI_ARGMAX on acc * inv_temp + Gumbel noise (temperature sampling)
 };
 
 struct GemmArgs {
@@ -102,6 +103,10 @@ struct GemmArgs {
   // EPI_ARGMAX
   unsigned long long *amax_keys;  // [M_max][amax_slots]: per-row maxima of column ranges
   int amax_slots;                 // row stride of amax_keys, at least gemm_argmax_slots()
+  // EPI_SAMPLE: noise of column c at row t is keyed by (seed, row_req[t], row_pos[t], c)
+  float inv_temp;
+  uint32_t seed_lo, seed_hi;
+  const int32_t *row_req, *row_pos;
   float *logits;                  // optional [M][N] float32
   long long ld_logits;
   // split-K (EPI_RESID_F32 / EPI_STORE_F32): partial tiles [splits][M_max][N] float32

@@ -63,6 +63,36 @@ __device__ __forceinline__ uint32_t orderable(float v) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// Philox4x32 with ten rounds (Salmon, Moraes, Dror, Shaw, SC 2011): each round
+// multiplies words 0 and 2 by the two Philox constants and mixes the high and
+// low halves with words 1 and 3 and the key; the key advances by the two Weyl
+// constants between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+// Standard Gumbel variate -ln(-ln u) for u = (w + 0.5) / 2^32; -ln u is taken
+// from 1 - u (exact in float) when u >= 1/2, so it stays accurate near u = 1.
+__device__ __forceinline__ float gumbel_of(uint32_t w) {
+  float t;
+  if (w < 0x80000000u) {
+    t = -logf(((float)w + 0.5f) * 0x1p-32f);
+  } else {
+    t = -log1pf(-(((float)(0xffffffffu - w) + 0.5f) * 0x1p-32f));
+  }
+  return -logf(t);
+}
+
 // LDS chunk swizzle of row r: 16 consecutive rows of one chunk column land in
 // 16 different 16-byte bank groups, and so do any 8 consecutive rows.
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & (CPR - 1); }
@@ -399,7 +429,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
             if (gm < Mlim) qkv_emit(a, gm, head, j, acc[i][2 * p][r], acc[i][2 * p + 1][r]);
           }
         }
-    } else if constexpr (EPI == EPI_ARGMAX) {
+    } else if constexpr (EPI == EPI_ARGMAX || EPI == EPI_SAMPLE) {
       // One key per row and wave column range (WN * 32 columns), stored and
       // merged by a later pass.  Each lane first takes the maximum over its WN
       // columns; the 32 column keys of each of 32 rows then go through LDS (idle
@@ -428,11 +458,25 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
         // a strictly larger order key replaces, so the lowest column wins ties
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
+          float noise[WN];
+          if constexpr (EPI == EPI_SAMPLE) {
+            // one Philox call per row and lane covers this lane's WN columns:
+            // counter (32 (c >> 7) + (c & 31), pos, req, 0), word (c >> 5) & 3
+            const int gm = min(rbase + i * 32 + 8 * (r >> 2) + (r & 3), a.M_max - 1);
+            const uint4 w = philox4x32_10(make_uint4((uint32_t)(32 * (col0 >> 7) + l32), (uint32_t)a.row_pos[gm],
+                                                     (uint32_t)a.row_req[gm], 0u), a.seed_lo, a.seed_hi);
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+            const int w0 = (col0 >> 5) & 3;
+#pragma unroll
+            for (int j = 0; j < WN; ++j) noise[j] = gumbel_of(ws[(w0 + j) & 3]);
+          }
           uint32_t bo = 0u, bc = 0xffffffffu;
 #pragma unroll
           for (int j = 0; j < WN; ++j) {
             const uint32_t c = (uint32_t)(col0 + 32 * j);
-            const uint32_t o = c < (uint32_t)a.N ? orderable(acc[i][j][r]) : 0u;
+            float v = acc[i][j][r];
+            if constexpr (EPI == EPI_SAMPLE) v = v * a.inv_temp + noise[j];
+            const uint32_t o = c < (uint32_t)a.N ? orderable(v) : 0u;
             const bool up = o > bo;
             bo = up ? o : bo;
             bc = up ? c : bc;
@@ -542,7 +586,9 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   const int nMT = a.tiles ? a.m_tiles : (a.M_max + T::TM - 1) / T::TM;
   const int nNT = EPI == EPI_SWIGLU ? (a.swiglu_inter + T::TN / 2 - 1) / (T::TN / 2) : (a.N + T::TN - 1) / T::TN;
   const int splits = a.splits > 1 ? a.splits : 1;
-  if (EPI == EPI_ARGMAX && (!a.amax_keys || a.amax_slots < nNT * T::GN)) return DCUT_EINVAL;
+  if ((EPI == EPI_ARGMAX || EPI == EPI_SAMPLE) && (!a.amax_keys || a.amax_slots < nNT * T::GN))
+    return DCUT_EINVAL;
+  if (EPI == EPI_SAMPLE && (!a.row_req || !a.row_pos || !(a.inv_temp >= 0.0f))) return DCUT_EINVAL;
   if (splits > 1 && ((EPI != EPI_RESID_F32 && EPI != EPI_STORE_F32 && EPI != EPI_QKV_ROPE) || a.tiles ||
                      !a.split_part || a.N % 4 || (EPI != EPI_QKV_ROPE && a.ldo % 4)))
     return DCUT_EINVAL;
@@ -608,6 +654,7 @@ int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {
     case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(kid, a, s);
     case EPI_QKV_ROPE: return launch_epi<EPI_QKV_ROPE>(kid, a, s);
     case EPI_ARGMAX: return launch_epi<EPI_ARGMAX>(kid, a, s);
+    case EPI_SAMPLE: return launch_epi<EPI_SAMPLE>(kid, a, s);
     case EPI_STORE_F32: return launch_epi<EPI_STORE_F32>(kid, a, s);
   }
   return DCUT_EINVAL;

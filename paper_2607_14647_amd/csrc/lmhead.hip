@@ -1,4 +1,5 @@
 // dcut_lm_head_argmax: final RMSNorm, LM-head GEMM with a fused row argmax.
+// dcut_lm_head_sample: the same with temperature sampling (Gumbel-max) fused in.
 //
 // The GEMM epilogue reduces each row's column ranges of the vocabulary (64 or
 // 128 columns, by tile shape) to one 64-bit key each (order-preserving logit
@@ -55,12 +56,14 @@ k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int strid
 
 using namespace dcut;
 
-extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
-                                   const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
-                                   int32_t *argmax, float *max_logit, float *logits, void *ws,
-                                   size_t ws_bytes, hipStream_t stream) {
+// Final norm, LM-head GEMM with the argmax (epi EPI_ARGMAX) or sampling
+// (EPI_SAMPLE) epilogue, then the per-row merge of the partial keys.
+static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *cu, const float *x,
+                       const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm, const int32_t *row_req,
+                       const int32_t *row_pos, float inv_temp, uint64_t seed, int32_t *token, float *max_score,
+                       float *logits, void *ws, size_t ws_bytes, hipStream_t stream) {
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
-  if (!cu || !x || !final_norm || !w_lm || !argmax || !(eps >= 0.0f)) return DCUT_EINVAL;
+  if (!cu || !x || !final_norm || !w_lm || !token || !(eps >= 0.0f)) return DCUT_EINVAL;
   const size_t need = lmhead_ws_bytes(H, V, B, D);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
@@ -74,8 +77,29 @@ extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu
   g.A = f; g.lda = H; g.K = H; g.M_max = M; g.m_count = Kstar;
   g.W = w_lm; g.ldw = H; g.N = V;
   g.amax_keys = keys; g.amax_slots = slots; g.logits = logits; g.ld_logits = V;
+  g.row_req = row_req; g.row_pos = row_pos; g.inv_temp = inv_temp;
+  g.seed_lo = (uint32_t)seed; g.seed_hi = (uint32_t)(seed >> 32);
   const int used = gemm_argmax_slots(g);
-  DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, EPI_ARGMAX, g, stream));
+  DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, epi, g, stream));
   return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3(M), dim3(256), 0, stream,
-                (const unsigned long long *)keys, used, slots, Kstar, M, argmax, max_logit);
+                (const unsigned long long *)keys, used, slots, Kstar, M, token, max_score);
+}
+
+extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
+                                   const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
+                                   int32_t *argmax, float *max_logit, float *logits, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  return lm_head_run(EPI_ARGMAX, H, V, B, D, cu, x, final_norm, eps, w_lm, nullptr, nullptr, 0.0f, 0, argmax,
+                     max_logit, logits, ws, ws_bytes, stream);
+}
+
+extern "C" int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu, const int32_t *packed_req,
+                                   const int32_t *packed_pos, const float *x, const dcut_bf16 *final_norm,
+                                   float eps, const dcut_bf16 *w_lm, float temperature, uint64_t seed,
+                                   int32_t *token, float *max_score, void *ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  if (!packed_req || !packed_pos || !(temperature > 0.0f) || !(temperature < __builtin_inff()))
+    return DCUT_EINVAL;
+  return lm_head_run(EPI_SAMPLE, H, V, B, D, cu, x, final_norm, eps, w_lm, packed_req, packed_pos,
+                     1.0f / temperature, seed, token, max_score, nullptr, ws, ws_bytes, stream);
 }

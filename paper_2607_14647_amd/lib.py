@@ -22,7 +22,7 @@ KERNELS = dict(NONE=0, SELECT=1, PACK=2, NORM=3, GEMM_QKV=4, ATTN=5, ATTN_COMBIN
                GEMM_GATE_UP=8, GEMM_DOWN=9, MOE=10, LM_HEAD=11, ARGMAX_FINAL=12, ACCEPT=13)
 
 EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",
-           "dcut_workspace_bytes", "dcut_strerror", "dcut_budgets_from_ratios",
+           "dcut_lm_head_sample", "dcut_workspace_bytes", "dcut_strerror", "dcut_budgets_from_ratios",
            "dcut_nearest_batch", "dcut_profile_arm"]
 
 
@@ -60,6 +60,8 @@ def _load() -> C.CDLL:
     lib.dcut_verify_layer.argtypes = [C.POINTER(LayerCfg), C.POINTER(LayerW), i32, i32, vp, vp, vp, vp,
                                       vp, vp, C.POINTER(KV), vp, vp, vp, sz, vp]
     lib.dcut_lm_head_argmax.argtypes = [i32, i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp, sz, vp]
+    lib.dcut_lm_head_sample.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, C.c_float, vp, C.c_float,
+                                        C.c_uint64, vp, vp, vp, sz, vp]
     lib.dcut_accept.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.dcut_workspace_bytes.argtypes = [i32, C.POINTER(LayerCfg), i32, i32]
     lib.dcut_workspace_bytes.restype = sz
@@ -68,7 +70,7 @@ def _load() -> C.CDLL:
     lib.dcut_budgets_from_ratios.argtypes = [i32, i32, i32, vp, vp, vp]
     lib.dcut_nearest_batch.argtypes = [i32, i32, vp]
     lib.dcut_profile_arm.argtypes = [i32, vp, vp]
-    for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",
+    for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_sample", "dcut_accept",
               "dcut_budgets_from_ratios", "dcut_nearest_batch", "dcut_profile_arm"]:
         getattr(lib, f).restype = i32
     return lib
@@ -184,6 +186,17 @@ def lm_head_argmax(H: int, V: int, B: int, D: int, cu: torch.Tensor, x: torch.Te
                                   _p(argmax), _p(max_logit), _p(logits), _p(ws),
                                   ws.numel() * ws.element_size(), _stream(stream))
     _check(st, "dcut_lm_head_argmax")
+
+
+def lm_head_sample(H: int, V: int, B: int, D: int, cu: torch.Tensor, packed_req: torch.Tensor,
+                   packed_pos: torch.Tensor, x: torch.Tensor, final_norm: torch.Tensor, eps: float,
+                   w_lm: torch.Tensor, temperature: float, seed: int, token: torch.Tensor, ws: torch.Tensor,
+                   max_score: Optional[torch.Tensor] = None, stream=None) -> None:
+    st = _lib.dcut_lm_head_sample(H, V, B, D, _p(cu), _p(packed_req), _p(packed_pos), _p(x), _p(final_norm),
+                                  float(eps), _p(w_lm), float(temperature), int(seed) & 0xFFFFFFFFFFFFFFFF,
+                                  _p(token), _p(max_score), _p(ws), ws.numel() * ws.element_size(),
+                                  _stream(stream))
+    _check(st, "dcut_lm_head_sample")
 
 
 def accept(B: int, D: int, draft: torch.Tensor, keep_len: torch.Tensor, cu: torch.Tensor,

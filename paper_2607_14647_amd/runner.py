@@ -49,6 +49,8 @@ class VerifyStep:
         self.total = torch.zeros(1, **i32)
         self.ws_layer = L.workspace(L.workspace_bytes(1, self.lcfg, self.B, self.D), device)
         self.ws_lm = L.workspace(L.workspace_bytes(2, self.lcfg, self.B, self.D), device)
+        self.temperature = 0.0      # > 0: temperature sampling instead of the greedy argmax
+        self.seed = 0
 
     def set_draft(self, draft: np.ndarray) -> None:
         self.draft.copy_(torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)))
@@ -62,6 +64,14 @@ class VerifyStep:
                        self.ws_layer, x_in=x_in, dev_err=self.dev_err)
 
     def lm_head(self, logits: Optional[torch.Tensor] = None) -> None:
+        """Target token of every kept row into `argmax`: the greedy argmax, or a
+        temperature-T draw when `self.temperature` > 0 (seeded by `self.seed`)."""
+        if self.temperature > 0.0:
+            L.lm_head_sample(self.ly.hidden, self.ly.vocab, self.B, self.D, self.sel["cu"],
+                             self.sel["packed_req"], self.sel["packed_pos"], self.x, self.w["final_norm"],
+                             self.ly.rms_eps, self.w["w_lm"], self.temperature, self.seed, self.argmax,
+                             self.ws_lm, max_score=self.max_logit)
+            return
         L.lm_head_argmax(self.ly.hidden, self.ly.vocab, self.B, self.D, self.sel["cu"], self.x,
                          self.w["final_norm"], self.ly.rms_eps, self.w["w_lm"], self.argmax,
                          self.ws_lm, max_logit=self.max_logit, logits=logits)

@@ -103,6 +103,16 @@ def test_other_entry_points_reject_invalid_args():
                                    fake, 1 << 30, None) == L.EINVAL
     assert lib.dcut_lm_head_argmax(4096, 10, 4, 15, fake, fake, fake, 1e-5, fake, fake, None, None,
                                    None, 0, None) == L.EWORKSPACE
+    # temperature sampling: null request/position arrays, non-positive or infinite temperature
+    smp = lambda req, pos, T, wsb: lib.dcut_lm_head_sample(4096, 10, 4, 15, fake, req, pos, fake, fake, 1e-5,
+                                                           fake, T, 7, fake, None, fake, wsb, None)
+    assert smp(None, fake, 1.0, 1 << 30) == L.EINVAL
+    assert smp(fake, None, 1.0, 1 << 30) == L.EINVAL
+    assert smp(fake, fake, 0.0, 1 << 30) == L.EINVAL
+    assert smp(fake, fake, -1.0, 1 << 30) == L.EINVAL
+    assert smp(fake, fake, float("inf"), 1 << 30) == L.EINVAL
+    assert smp(fake, fake, float("nan"), 1 << 30) == L.EINVAL
+    assert smp(fake, fake, 1.0, 0) == L.EWORKSPACE
     cfg = L.LayerCfg(256, 4, 2, 64, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
     w = L.LayerW(*([0x1000] * 7 + [None] * 3))
     kv = L.KV(0x1000, 0x1000, 0x1000, 0x1000)
