@@ -155,6 +155,11 @@ def main():
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the timed region, run a plain device-to-device copy of this many bytes "
                          "three times (reference kernel for scaling HBM byte counters)")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="target decoding: 0 = greedy (default), T > 0 = temperature-T sampling through "
+                         "dcut_lm_head_sample (the paper's temperature-1 regime); drafts are forced from "
+                         "the same sampled tokens")
+    ap.add_argument("--sample-seed", type=int, default=1, help="seed of the sampling noise")
     ap.add_argument("--state", default=None,
                     help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
                          "run of the same workload; written when missing, reused when present (a "
@@ -182,12 +187,14 @@ def main():
     kv = wl.make_kv(cfg, args.seed, st["ctx_len"])
     log(f"generated in {time.time() - t0:.1f}s; uploading")
     vs = runner.VerifyStep(cfg, w, st, kv)
+    vs.temperature, vs.seed = float(args.temperature), int(args.sample_seed)
     torch.cuda.synchronize()
     budgets = list(cfg.budgets)
     state = None
     if args.state and os.path.exists(args.state):
         state = json.load(open(args.state))
         assert state["workload"] == [cfg.cid, args.seed] and state["budgets"] == budgets, "state mismatch"
+        assert state.get("temperature", 0.0) == args.temperature, "state mismatch (temperature)"
         vs.set_draft(np.array(state["draft"], dtype=np.int32))
         log(f"reusing forced drafts, cost row and dominant kernel from {args.state}")
     else:
@@ -240,7 +247,7 @@ def main():
         breakdown[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
     dominant = max(breakdown, key=lambda k: breakdown[k])
     if args.state and state is None:
-        json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms,
+        json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,
                        accepted_per_budget=acc_per_k, kernel_us=breakdown,
                        draft=vs.host("draft").tolist()), open(args.state, "w"))
     log("kernel us: " + ", ".join(f"{k}={v}" for k, v in breakdown.items()) + f"; dominant {dominant}")
@@ -307,7 +314,9 @@ def main():
                              f"{ly.n_q}q/{ly.n_kv}kv hd{ly.head_dim}, I={ly.inter}, V={ly.vocab}, "
                              f"L~{cfg.ctx}, conf {cfg.conf_model}; seed {args.seed}",
                     global_batch=cfg.B, K_star=Kstar, r_star=rstar, accepted_per_step=accepted,
-                    budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm"),
+                    budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm",
+                    target_decoding="greedy" if args.temperature == 0 else
+                    f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})"),
         hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         step_algorithmic_bytes=int(step_bytes),
         roofline=rl,
@@ -317,7 +326,7 @@ def main():
         fixed_ratio=fixed,
         source_hash=source_hash(),
     )
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.temperature == 0:
         out["cpu_baseline"] = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
     else:
         out["cpu_baseline"] = None

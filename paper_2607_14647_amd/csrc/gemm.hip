@@ -33,6 +33,8 @@
 //   SWIGLU    groups (2p, 2p+1) = (gate rows, up rows) of the same 32 outputs;
 //   QKV_ROPE  groups (2p, 2p+1) = the two halves (j, j + hd/2) of RoPE pairs.
 
+#include <type_traits>
+
 #include "dcut_internal.h"
 
 namespace dcut {
@@ -74,23 +76,29 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
       k0 += 0x9E3779B9u;
       k1 += 0xBB67AE85u;
     }
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x, p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0);
   }
   return c;
 }
 
-// Standard Gumbel variate -ln(-ln u) for u = (w + 0.5) / 2^32; -ln u is taken
-// from 1 - u (exact in float) when u >= 1/2, so it stays accurate near u = 1.
+// Standard Gumbel variate -ln(-ln u) for u = (w + 0.5) / 2^32, with the
+// hardware base-2 logarithm (v_log_f32, about one ulp).  t = -ln u comes from u
+// itself when u < 1/2; otherwise from x = 1 - u (exact in float): by the series
+// x + x^2/2 + x^3/3 + x^4/4 when x < 1/32 (relative error below x^4/5 < 2^-22),
+// else as -ln(1 - x) with 1 - x rounded (relative error below 2^-24 / x <=
+// 2^-19).  t so keeps its relative accuracy as u approaches 1, where the
+// largest variates come from.  Both branches share one logarithm and are
+// selected per lane, so lanes never diverge, and nothing divides.
 __device__ __forceinline__ float gumbel_of(uint32_t w) {
-  float t;
-  if (w < 0x80000000u) {
-    t = -logf(((float)w + 0.5f) * 0x1p-32f);
-  } else {
-    t = -log1pf(-(((float)(0xffffffffu - w) + 0.5f) * 0x1p-32f));
-  }
-  return -logf(t);
+  constexpr float LN2 = 0.6931471805599453f;
+  const bool lo = w < 0x80000000u;
+  const float u = ((float)w + 0.5f) * 0x1p-32f;
+  const float x = ((float)(0xffffffffu - w) + 0.5f) * 0x1p-32f;
+  const float l = __log2f(lo ? u : 1.0f - x) * LN2;    // one logarithm for either branch
+  const float s = x * (1.0f + x * (0.5f + x * (1.0f / 3.0f + x * 0.25f)));
+  const float t = (lo || x >= 0x1p-5f) ? -l : s;
+  return -__log2f(t) * LN2;
 }
 
 // LDS chunk swizzle of row r: 16 consecutive rows of one chunk column land in
@@ -452,8 +460,11 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
                 if (col0 + 32 * j < a.N) a.logits[(size_t)gm * a.ld_logits + col0 + 32 * j] = acc[i][j][r];
           }
       }
-#pragma unroll
-      for (int i = 0; i < WM; ++i) {
+      // the row blocks go through a compile-time index: a plain loop over them
+      // is too large to unroll once sampling is fused in, and a run-time index
+      // into acc would move the accumulators to scratch memory
+      auto row_block = [&](auto ic) {
+        constexpr int i = decltype(ic)::value;
         // branch-free per-lane maximum over the WN columns (increasing with j):
         // a strictly larger order key replaces, so the lowest column wins ties
 #pragma unroll
@@ -465,10 +476,13 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
             const int gm = min(rbase + i * 32 + 8 * (r >> 2) + (r & 3), a.M_max - 1);
             const uint4 w = philox4x32_10(make_uint4((uint32_t)(32 * (col0 >> 7) + l32), (uint32_t)a.row_pos[gm],
                                                      (uint32_t)a.row_req[gm], 0u), a.seed_lo, a.seed_hi);
-            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
             const int w0 = (col0 >> 5) & 3;
 #pragma unroll
-            for (int j = 0; j < WN; ++j) noise[j] = gumbel_of(ws[(w0 + j) & 3]);
+            for (int j = 0; j < WN; ++j) {
+              const int k = (w0 + j) & 3;     // selects, not an indexed array (which would live in scratch)
+              const uint32_t wk = k == 0 ? w.x : k == 1 ? w.y : k == 2 ? w.z : w.w;
+              noise[j] = gumbel_of(wk);
+            }
           }
           uint32_t bo = 0u, bc = 0xffffffffu;
 #pragma unroll
@@ -498,7 +512,12 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
         }
         __builtin_amdgcn_wave_barrier();
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      }
+      };
+      static_assert(WM >= 1 && WM <= 4, "row blocks per wave");
+      row_block(std::integral_constant<int, 0>{});
+      if constexpr (WM > 1) row_block(std::integral_constant<int, 1>{});
+      if constexpr (WM > 2) row_block(std::integral_constant<int, 2>{});
+      if constexpr (WM > 3) row_block(std::integral_constant<int, 3>{});
       // the next task's prologue refills the LDS this pass used
       ring_barrier();
     }
