@@ -21,7 +21,9 @@ Modules
   sampling -- temperature-T target sampling (Gumbel-max over Philox4x32-10
              uniforms), the paper's temperature-1 regime
   accept  -- greedy target-only longest-prefix acceptance (Sec. 3.2, App. A)
+  rs      -- the rejection-sampling extension of App. B: shifted scores,
+             causal budget selection, RS acceptance with residual sampling
   drafts  -- forced-match draft construction for tests and benchmarks
 """
 from .errors import DcutArgError, DcutDataError, DERR_CONF, DERR_TOKEN, DERR_CAPACITY  # noqa: F401
-from . import select, layer, lm_head, accept, sampling  # noqa: F401
+from . import select, layer, lm_head, accept, sampling, rs  # noqa: F401
