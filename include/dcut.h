@@ -14,6 +14,12 @@
  *
  *   dcut_lm_head_sample  final norm, LM head and a Gumbel-max draw per kept row
  *
+ * and, for drafters that expose their proposal distributions and targets that
+ * verify by rejection sampling (App. B), replacements of the first and last:
+ *
+ *   dcut_select_rs       shifted scores with a causal budget choice
+ *   dcut_accept_rs       RS acceptance with residual sampling
+ *
  * Conventions shared by every call
  *   - All pointers marked "dev" are device pointers on the current HIP device;
  *     "host" pointers are read during the call only.  The caller owns every
@@ -102,6 +108,44 @@ int dcut_select(int B, int D, const float *conf, const int32_t *draft, const int
                 int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
                 int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
                 hipStream_t stream);
+
+/*
+ * dcut_select_rs -- RS-safe selection (App. B, causality under rejection sampling).
+ *
+ * As dcut_select, with two changes that keep whether a position is verified
+ * independent of its own proposal:
+ *   - positions are ranked by the shifted scores of Eq. dcut-shifted-score,
+ *     s~_{i,0} = s~_{i,1} = 1 and s~_{i,k} = s~_{i,k-1} * c_{i,k-1} (float32, in
+ *     depth order), with the same ties (smaller depth, then smaller request);
+ *   - the budget is chosen causally:
+ *     DCUT_RS_SCAN   the early-stopping scan.  Positions are admitted in rank
+ *                    order from K = B (every bonus position) while the
+ *                    objective strictly rises: K* is the first K >= B with
+ *                    J(K+1) <= J(K), or B(D+1).  J(K) = P(K) * 2^-40 / C(K),
+ *                    P(K) the exact sum of trunc(s~ * 2^40) over the first K
+ *                    ranks, and C(K) the cost table interpolated linearly
+ *                    between consecutive budgets (K_r, C_r), flat outside
+ *                    [K_0, K_{R-1}], the last of equal budgets holding at K_r:
+ *                    C(K) = C_r + ((C_{r+1} - C_r) * (K - K_r)) / (K_{r+1} - K_r),
+ *                    float64 in that order.  choice = {K*, the last r with
+ *                    K_r <= K*, or -1}.
+ *     DCUT_RS_FIXED  a budget fixed before the block was drafted (for example
+ *                    from earlier steps' statistics): R must be 1 and K* = K_0,
+ *                    the global top-K_0 of the shifted scores; choice = {K_0, 0}.
+ * The proposals' conditional distributions q must be the ones the
+ * confidences come from: c_{i,k} = q_{i,k}(z_{i,k}).
+ *
+ *   mode      DCUT_RS_SCAN or DCUT_RS_FIXED
+ *   every other argument as for dcut_select (benefit[r] sums shifted scores)
+ * Returns DCUT_OK, DCUT_EINVAL (also for an unknown mode, or R != 1 with
+ * DCUT_RS_FIXED), DCUT_EHIP.
+ */
+enum { DCUT_RS_SCAN = 0, DCUT_RS_FIXED = 1 };
+int dcut_select_rs(int B, int D, const float *conf, const int32_t *draft, const int32_t *ctx_len,
+                   int mode, int R, const int32_t *budgets, const double *costs,
+                   int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
+                   int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                   hipStream_t stream);
 
 /* Shape of one decoder layer.  n_exp == 0 selects the dense SwiGLU MLP of width
  * `inter`; n_exp > 0 selects a routed MoE with top_k experts of width exp_inter.
@@ -208,15 +252,20 @@ int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const flo
  *   temperature             > 0 and finite
  *   token     dev [B(D+1)] int32 out;   max_score dev [B(D+1)] float32 out (nullable):
  *             the winning logits / T + G
+ *   logits    dev [B(D+1)][V] float32 out (nullable): the raw logits of rows < K*
+ *   lse       dev [B(D+1)] float32 out (nullable; needs logits):
+ *             ln sum_c exp(logits[t][c] * (1/T)), the row's log-partition
+ *             function (dcut_accept_rs takes logits and lse)
  *   other arguments and the workspace as for dcut_lm_head_argmax
- * Errors: DCUT_EINVAL for a null request/position array or a temperature that
- * is not positive and finite, otherwise as dcut_lm_head_argmax.
+ * Errors: DCUT_EINVAL for a null request/position array, a temperature that
+ * is not positive and finite, or lse without logits; otherwise as
+ * dcut_lm_head_argmax.
  */
 int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu, const int32_t *packed_req,
                         const int32_t *packed_pos, const float *x, const dcut_bf16 *final_norm,
                         float eps, const dcut_bf16 *w_lm, float temperature, uint64_t seed,
-                        int32_t *token, float *max_score, void *ws, size_t ws_bytes,
-                        hipStream_t stream);
+                        int32_t *token, float *max_score, float *logits, float *lse, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
 
 /*
  * dcut_accept -- greedy target-only acceptance (Sec. 3.2, App. A).
@@ -233,8 +282,45 @@ int dcut_accept(int B, int D, const int32_t *draft, const int32_t *keep_len, con
                 const int32_t *argmax, int32_t *accept_len, int32_t *next_tok, int32_t *total,
                 int32_t *ctx_len_inout, hipStream_t stream);
 
-/* Scratch bytes for call `which` (0 select, 1 verify_layer, 2 lm_head_argmax,
- * 3 accept); cfg may be NULL for 0 and 3.  Returns 0 when none is needed and
+/*
+ * dcut_accept_rs -- rejection-sampling acceptance (App. B, distributional correctness).
+ *
+ * Request i verifies its kept drafts in order.  Draft z = draft[i][j] is
+ * checked at row r = cu[i] + j - 1 against p_r = softmax(logits[r] / T):
+ * accepted when u_r * q[i][j-1][z] < p_r(z) (float64; probability
+ * min(1, p/q)), with u_r = (w + 0.5) / 2^32, w word 0 of Philox4x32-10 at
+ * counter (0, packed_pos[r], i, 1) under `seed`.  At the first rejection the
+ * committed token is argmax_c ln((p_r(c) - q[i][j-1][c])_+) + G(r, c), G the
+ * row's Gumbel noise of dcut_lm_head_sample (same seed), or token[r] if no
+ * column has p_r(c) > q[i][j-1][c]; when every kept draft is accepted it is
+ * token[cu[i] + n_i], the target's own draw.  p in the residual is float32.
+ *
+ *   V, temperature, seed   as given to dcut_lm_head_sample for the same rows
+ *   draft      dev [B][D+1] int32; q dev [B][D][V] float32, q[i][k-1] = the
+ *              proposal distribution of z_{i,k}
+ *   keep_len, cu, packed_pos  dev, from the selection call
+ *   logits     dev [B(D+1)][V] float32, lse dev [B(D+1)] float32, token dev
+ *              [B(D+1)] int32: the outputs of dcut_lm_head_sample
+ *   accept_len dev [B] out; next_tok dev [B] out; total dev [1] out: sum (a_i + 1)
+ *   ctx_len_inout dev [B], nullable: incremented by a_i + 1
+ *   ws         dev scratch of dcut_workspace_bytes(4, cfg with vocab = V, B, D)
+ *              bytes, 256-byte aligned
+ *   dev_err    nullable; DCUT_DERR_TOKEN for a draft outside [0, V), which is
+ *              then rejected
+ * Only the rows a request consults are read: the rejecting row's logits and
+ * q[i][j-1] in full, one column of the others.
+ * Returns DCUT_OK, DCUT_EINVAL, DCUT_EWORKSPACE, DCUT_EHIP.
+ */
+int dcut_accept_rs(int B, int D, int V, float temperature, uint64_t seed, const int32_t *draft,
+                   const float *q, const int32_t *keep_len, const int32_t *cu,
+                   const int32_t *packed_pos, const float *logits, const float *lse,
+                   const int32_t *token, int32_t *accept_len, int32_t *next_tok, int32_t *total,
+                   int32_t *ctx_len_inout, void *ws, size_t ws_bytes, int32_t *dev_err,
+                   hipStream_t stream);
+
+/* Scratch bytes for call `which` (0 select and select_rs, 1 verify_layer,
+ * 2 lm_head_argmax and lm_head_sample, 3 accept, 4 accept_rs, which reads
+ * cfg->vocab); cfg may be NULL for 0 and 3.  Returns 0 when none is needed and
  * (size_t)-1 for invalid shapes. */
 size_t dcut_workspace_bytes(int which, const dcut_layer_cfg *cfg, int B, int D);
 
@@ -258,7 +344,8 @@ enum {
   DCUT_KERNEL_NONE = 0, DCUT_KERNEL_SELECT, DCUT_KERNEL_PACK, DCUT_KERNEL_NORM,
   DCUT_KERNEL_GEMM_QKV, DCUT_KERNEL_ATTN, DCUT_KERNEL_ATTN_COMBINE, DCUT_KERNEL_GEMM_O,
   DCUT_KERNEL_GEMM_GATE_UP, DCUT_KERNEL_GEMM_DOWN, DCUT_KERNEL_MOE, DCUT_KERNEL_LM_HEAD,
-  DCUT_KERNEL_ARGMAX_FINAL, DCUT_KERNEL_ACCEPT
+  DCUT_KERNEL_ARGMAX_FINAL, DCUT_KERNEL_ACCEPT, DCUT_KERNEL_RS_DECIDE, DCUT_KERNEL_RS_RESIDUAL,
+  DCUT_KERNEL_RS_FINISH
 };
 int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop);
 

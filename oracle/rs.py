@@ -121,18 +121,18 @@ def causal_scan(s: np.ndarray, curve: np.ndarray) -> Dict[str, object]:
     P = int(u[:, 0].astype(object).sum())
     J = _objective(P, curve[K])
     order = [(i, 0) for i in range(B)]
+    req = np.arange(B)
     while True:
-        best = None
-        for i in range(B):
-            k = int(frontier[i])
-            if k >= D1:
-                continue
-            key = (-float(s[i, k]), k, i)
-            if best is None or key < best[0]:
-                best = (key, i, k)
-        if best is None:
+        live = frontier < D1
+        if not live.any():
             break
-        _, i, k = best
+        # the frontier with the largest score; ties to the smaller depth, then request
+        f = np.minimum(frontier, D1 - 1)
+        sc = np.where(live, s[req, f].astype(np.float64), -1.0)
+        top = sc == sc.max()
+        dep = np.where(top, f, D1)
+        i = int(np.flatnonzero(top & (dep == dep.min()))[0])
+        k = int(frontier[i])
         P2 = P + int(u[i, k])
         J2 = _objective(P2, curve[K + 1])
         if not J2 > J:

@@ -5,6 +5,7 @@
 namespace dcut {
 size_t layer_ws_bytes(const dcut_layer_cfg *c, int B, int D);
 size_t lmhead_ws_bytes(int H, int V, int B, int D);
+size_t accept_rs_ws_bytes(int V, int B);
 
 ProfileHook &profile_hook() {
   static thread_local ProfileHook h = {DCUT_KERNEL_NONE, nullptr, nullptr};
@@ -34,6 +35,9 @@ extern "C" size_t dcut_workspace_bytes(int which, const dcut_layer_cfg *cfg, int
       if (!cfg || cfg->hidden <= 0 || cfg->hidden % 8 || cfg->vocab <= 0) return (size_t)-1;
       return lmhead_ws_bytes(cfg->hidden, cfg->vocab, B, D);
     case 3: return 0;
+    case 4:
+      if (!cfg || cfg->vocab <= 0) return (size_t)-1;
+      return accept_rs_ws_bytes(cfg->vocab, B);
   }
   return (size_t)-1;
 }
@@ -64,7 +68,7 @@ extern "C" int dcut_nearest_batch(int B, int n, const int32_t *captured) {
 }
 
 extern "C" int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop) {
-  if (kernel < DCUT_KERNEL_NONE || kernel > DCUT_KERNEL_ACCEPT) return DCUT_EINVAL;
+  if (kernel < DCUT_KERNEL_NONE || kernel > DCUT_KERNEL_RS_FINISH) return DCUT_EINVAL;
   if (kernel != DCUT_KERNEL_NONE && (!start || !stop)) return DCUT_EINVAL;
   ProfileHook &h = profile_hook();
   h.kernel = kernel;

@@ -1,5 +1,7 @@
 // dcut_lm_head_argmax: final RMSNorm, LM-head GEMM with a fused row argmax.
-// dcut_lm_head_sample: the same with temperature sampling (Gumbel-max) fused in.
+// dcut_lm_head_sample: the same with temperature sampling (Gumbel-max) fused in,
+// optionally also writing the logits and each row's log-partition function
+// (what rejection-sampling verification needs).
 //
 // The GEMM epilogue reduces each row's column ranges of the vocabulary (64 or
 // 128 columns, by tile shape) to one 64-bit key each (order-preserving logit
@@ -19,12 +21,23 @@ size_t lmhead_ws_bytes(int H, int V, int B, int D) {
 
 namespace {
 
-// One workgroup per row: the maximum of the row's partial keys, decoded.
+// One workgroup per row: the maximum of the row's partial keys, decoded; with
+// `lse`, also ln sum_c exp(logits[c] * inv_temp) of the row's written logits
+// (an online maximum and rescaled sum per thread, merged across the group).
+__device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2) {
+  const float M = fmaxf(m, m2);
+  if (M == -__builtin_inff()) return;      // both empty
+  s = s * __expf(m - M) + s2 * __expf(m2 - M);
+  m = M;
+}
+
 __global__ void __launch_bounds__(256)
 k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int stride,
                const int32_t *__restrict__ m_count, int M_max, int32_t *__restrict__ argmax,
-               float *__restrict__ max_logit) {
+               float *__restrict__ max_logit, const float *__restrict__ logits, int V, float inv_temp,
+               float *__restrict__ lse) {
   __shared__ unsigned long long s_max[4];
+  __shared__ float s_m[4], s_s[4];
   const int t = blockIdx.x;
   if (t >= M_max || t >= *m_count) return;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -40,6 +53,34 @@ k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int strid
     k = o > k ? o : k;
   }
   if (lane == 0) s_max[tid >> 6] = k;
+  if (lse) {
+    float m = -__builtin_inff(), sum = 0.0f;
+    const float *lr = logits + (size_t)t * V;
+    auto add = [&](float x) {
+      x *= inv_temp;
+      const float M = fmaxf(m, x);
+      sum = sum * __expf(m - M) + __expf(x - M);
+      m = M;
+    };
+    if ((V & 3) == 0) {
+      const float4 *l4 = (const float4 *)lr;
+      for (int c = tid; c < (V >> 2); c += 256) {
+        const float4 v = l4[c];
+        add(v.x); add(v.y); add(v.z); add(v.w);
+      }
+    } else {
+      for (int c = tid; c < V; c += 256) add(lr[c]);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float m2 = __shfl_xor(m, off, 64), s2 = __shfl_xor(sum, off, 64);
+      lse_merge(m, sum, m2, s2);
+    }
+    if (lane == 0) {
+      s_m[tid >> 6] = m;
+      s_s[tid >> 6] = sum;
+    }
+  }
   __syncthreads();
   if (tid != 0) return;
   for (int w = 1; w < 4; ++w) k = s_max[w] > k ? s_max[w] : k;
@@ -48,6 +89,11 @@ k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int strid
     uint32_t u = (uint32_t)(k >> 32);
     u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
     max_logit[t] = __uint_as_float(u);
+  }
+  if (lse) {
+    float m = s_m[0], sum = s_s[0];
+    for (int w = 1; w < 4; ++w) lse_merge(m, sum, s_m[w], s_s[w]);
+    lse[t] = m + __logf(sum);
   }
 }
 
@@ -61,9 +107,10 @@ using namespace dcut;
 static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *cu, const float *x,
                        const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm, const int32_t *row_req,
                        const int32_t *row_pos, float inv_temp, uint64_t seed, int32_t *token, float *max_score,
-                       float *logits, void *ws, size_t ws_bytes, hipStream_t stream) {
+                       float *logits, float *lse, void *ws, size_t ws_bytes, hipStream_t stream) {
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
   if (!cu || !x || !final_norm || !w_lm || !token || !(eps >= 0.0f)) return DCUT_EINVAL;
+  if (lse && !logits) return DCUT_EINVAL;
   const size_t need = lmhead_ws_bytes(H, V, B, D);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
@@ -82,7 +129,8 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   const int used = gemm_argmax_slots(g);
   DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, epi, g, stream));
   return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3(M), dim3(256), 0, stream,
-                (const unsigned long long *)keys, used, slots, Kstar, M, token, max_score);
+                (const unsigned long long *)keys, used, slots, Kstar, M, token, max_score,
+                (const float *)logits, V, inv_temp, lse);
 }
 
 extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
@@ -90,16 +138,16 @@ extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu
                                    int32_t *argmax, float *max_logit, float *logits, void *ws,
                                    size_t ws_bytes, hipStream_t stream) {
   return lm_head_run(EPI_ARGMAX, H, V, B, D, cu, x, final_norm, eps, w_lm, nullptr, nullptr, 0.0f, 0, argmax,
-                     max_logit, logits, ws, ws_bytes, stream);
+                     max_logit, logits, nullptr, ws, ws_bytes, stream);
 }
 
 extern "C" int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu, const int32_t *packed_req,
                                    const int32_t *packed_pos, const float *x, const dcut_bf16 *final_norm,
                                    float eps, const dcut_bf16 *w_lm, float temperature, uint64_t seed,
-                                   int32_t *token, float *max_score, void *ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+                                   int32_t *token, float *max_score, float *logits, float *lse, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
   if (!packed_req || !packed_pos || !(temperature > 0.0f) || !(temperature < __builtin_inff()))
     return DCUT_EINVAL;
   return lm_head_run(EPI_SAMPLE, H, V, B, D, cu, x, final_norm, eps, w_lm, packed_req, packed_pos,
-                     1.0f / temperature, seed, token, max_score, nullptr, ws, ws_bytes, stream);
+                     1.0f / temperature, seed, token, max_score, logits, lse, ws, ws_bytes, stream);
 }

@@ -1,8 +1,11 @@
 // Cross-request selection (scores, ranking, budget choice, keep depths) and packing.
 //
 // Sec. 3.2 Eq. dcut-prefix-score, Sec. 3.3 Eq. dcut-objective, Alg. 1 and the
-// packing of App. C.  Both kernels run as one 1024-thread workgroup: the whole
-// problem is at most 8192 positions (64 KB of sort keys in LDS), so a single
+// packing of App. C; for rejection-sampling verification (App. B) the same
+// kernel ranks the shifted scores of Eq. dcut-shifted-score and chooses the
+// budget causally: by the early-stopping scan, or as a budget fixed beforehand.
+// Both kernels run as one 1024-thread workgroup: the whole problem is at most
+// 8192 positions (64 KB of sort keys in LDS), so a single
 // workgroup avoids any grid-wide synchronisation and launch round trips.
 //
 // Bit-exactness: each request's scores are one sequential float32 product per
@@ -15,8 +18,12 @@
 
 namespace dcut {
 
+enum SelectMode { SEL_BUCKETS = 0, SEL_SCAN = 1, SEL_FIXED = 2 };
+
 struct SelectParams {
   int B, D, R;
+  int shift;      // 1: rank the shifted scores s~_{i,k} = s_{i,k-1} (s~_{i,1} = 1)
+  int mode;       // SelectMode
   int budgets[DCUT_MAX_CANDIDATES];
   double costs[DCUT_MAX_CANDIDATES];
 };
@@ -35,6 +42,26 @@ __device__ __forceinline__ unsigned long long key_units(unsigned long long key) 
 __device__ __forceinline__ bool conf_bad(float c) { return !(c >= 0.0f && c <= 1.0f) || signbit(c); }
 
 #pragma clang fp contract(off)
+// Step cost at an arbitrary verification size K for the causal scan: linear
+// between consecutive budgets (K_r, C_r), the end costs outside them, and the
+// last of several equal budgets at that K.  Same float64 operations, in the
+// same order, on every platform.
+__device__ double cost_at(const SelectParams &p, int K) {
+  int r = -1;
+  for (int t = 0; t < p.R; ++t)
+    if (p.budgets[t] <= K) r = t;
+  if (r < 0) return p.costs[0];
+  if (r == p.R - 1) return p.costs[p.R - 1];
+  const int ka = p.budgets[r], kb = p.budgets[r + 1];
+  const double ca = p.costs[r], cb = p.costs[r + 1];
+  return ca + ((cb - ca) * (double)(K - ka)) / (double)(kb - ka);
+}
+
+// objective of Eq. dcut-objective for the exact fixed-point benefit P
+__device__ __forceinline__ double objective(unsigned long long P, double cost) {
+  return ((double)P * 0x1p-40) / cost;
+}
+
 __global__ void __launch_bounds__(1024)
 k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ keep_len,
          int32_t *__restrict__ choice, unsigned long long *__restrict__ benefit,
@@ -43,7 +70,7 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   __shared__ unsigned long long s_wave[17];
   __shared__ unsigned long long s_ben[DCUT_MAX_CANDIDATES];
   __shared__ unsigned long long s_tau;
-  __shared__ int s_err;
+  __shared__ int s_err, s_stop;
 
   const int tid = threadIdx.x;
   const int D = p.D, D1 = p.D + 1, B = p.B;
@@ -52,7 +79,10 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   while (NP < N) NP <<= 1;
   unsigned long long *keys = smem;          // [NP]
   float *s_conf = (float *)(smem + NP + blockDim.x);   // [B * D], staged once (coalesced)
-  if (tid == 0) s_err = 0;
+  if (tid == 0) {
+    s_err = 0;
+    s_stop = N;
+  }
   for (int j = tid; j < B * D; j += blockDim.x) s_conf[j] = conf[j];
   __syncthreads();
 
@@ -66,8 +96,9 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
         s_err = 1;
         c = 0.0f;
       }
+      const float prev = s;          // the shifted score of depth k: the product up to k - 1
       s = s * c;
-      keys[i * D1 + k] = rank_key(s, k, i);
+      keys[i * D1 + k] = rank_key(p.shift ? prev : s, k, i);
     }
   }
   for (int j = N + tid; j < NP; j += blockDim.x) keys[j] = 0ull;   // sorts last
@@ -136,18 +167,46 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   }
   __syncthreads();
 
-  // 4. budget choice: first strict maximum of benefit * 2^-40 / cost
-  if (tid == 0) {
-    int best = 0;
-    double best_obj = -1.0;
-    for (int r = 0; r < p.R; ++r) {
-      double obj = ((double)s_ben[r] * 0x1p-40) / p.costs[r];
-      if (obj > best_obj) {
-        best_obj = obj;
-        best = r;
+  // 4a. causal scan (App. B): the positions enter in rank order from K = B on,
+  // and the scan stops at the first K whose next position does not strictly
+  // raise the objective.  Every thread tests the sizes of its own ranks.
+  if (p.mode == SEL_SCAN) {
+    unsigned long long P = s_pre[tid];          // benefit of the first tid * E ranks
+    int stop = N;
+    for (int m = tid * E; m < tid * E + E && m < N; ++m) {
+      const unsigned long long P1 = P + key_units(keys[m]);
+      if (m >= B && !(objective(P1, cost_at(p, m + 1)) > objective(P, cost_at(p, m)))) {
+        stop = m;
+        break;
       }
+      P = P1;
     }
-    int Kstar = p.budgets[best];
+    if (stop < N) atomicMin(&s_stop, stop);
+  }
+  __syncthreads();
+
+  // 4b. budget choice: the scan's stop, the fixed budget, or the first strict
+  // maximum of benefit * 2^-40 / cost over the candidates
+  if (tid == 0) {
+    int best = 0, Kstar;
+    if (p.mode == SEL_BUCKETS) {
+      double best_obj = -1.0;
+      for (int r = 0; r < p.R; ++r) {
+        double obj = objective(s_ben[r], p.costs[r]);
+        if (obj > best_obj) {
+          best_obj = obj;
+          best = r;
+        }
+      }
+      Kstar = p.budgets[best];
+    } else if (p.mode == SEL_FIXED) {
+      Kstar = p.budgets[0];
+    } else {
+      Kstar = s_stop;
+      best = -1;                      // the last candidate budget not above K*
+      for (int r = 0; r < p.R; ++r)
+        if (p.budgets[r] <= Kstar) best = r;
+    }
     choice[0] = Kstar;
     choice[1] = best;
     s_tau = keys[Kstar - 1];          // the K*-th largest key
@@ -163,8 +222,9 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
     for (int k = 1; k <= D; ++k) {
       float c = s_conf[i * D + (k - 1)];
       if (conf_bad(c)) c = 0.0f;
+      const float prev = s;
       s = s * c;
-      if (rank_key(s, k, i) >= tau) n = k + 1;
+      if (rank_key(p.shift ? prev : s, k, i) >= tau) n = k + 1;
       else break;
     }
     if (rank_key(1.0f, 0, i) < tau) n = 0;   // impossible when K* >= B; kept for safety
@@ -217,14 +277,14 @@ k_pack(int B, int D, const int32_t *__restrict__ keep_len, const int32_t *__rest
 
 using namespace dcut;
 
-extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft,
-                           const int32_t *ctx_len, int R, const int32_t *budgets,
-                           const double *costs, int32_t *keep_len, int32_t *cu,
-                           int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
-                           int32_t *choice, uint64_t *benefit, int32_t *dev_err,
-                           hipStream_t stream) {
+static int select_run(int B, int D, const float *conf, const int32_t *draft, const int32_t *ctx_len,
+                      int shift, int mode, int R, const int32_t *budgets, const double *costs,
+                      int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
+                      int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                      hipStream_t stream) {
   if (!batch_ok(B, D)) return DCUT_EINVAL;
   if (R < 1 || R > DCUT_MAX_CANDIDATES || !budgets || !costs) return DCUT_EINVAL;
+  if (mode == SEL_FIXED && R != 1) return DCUT_EINVAL;
   if (!conf && D > 0) return DCUT_EINVAL;
   if (!draft || !ctx_len || !keep_len || !cu || !packed_tok || !packed_pos || !packed_req || !choice)
     return DCUT_EINVAL;
@@ -232,6 +292,8 @@ extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft
   p.B = B;
   p.D = D;
   p.R = R;
+  p.shift = shift;
+  p.mode = mode;
   for (int r = 0; r < R; ++r) {
     int K = budgets[r];
     double c = costs[r];
@@ -249,4 +311,28 @@ extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft
   DCUT_TRY(launch(DCUT_KERNEL_PACK, k_pack, dim3(1), dim3(1024), 0, stream, B, D,
                   (const int32_t *)keep_len, draft, ctx_len, cu, packed_tok, packed_pos, packed_req));
   return DCUT_OK;
+}
+
+extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft,
+                           const int32_t *ctx_len, int R, const int32_t *budgets,
+                           const double *costs, int32_t *keep_len, int32_t *cu,
+                           int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
+                           int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                           hipStream_t stream) {
+  return select_run(B, D, conf, draft, ctx_len, 0, SEL_BUCKETS, R, budgets, costs, keep_len, cu,
+                    packed_tok, packed_pos, packed_req, choice, benefit, dev_err, stream);
+}
+
+extern "C" int dcut_select_rs(int B, int D, const float *conf, const int32_t *draft,
+                              const int32_t *ctx_len, int mode, int R, const int32_t *budgets,
+                              const double *costs, int32_t *keep_len, int32_t *cu,
+                              int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
+                              int32_t *choice, uint64_t *benefit, int32_t *dev_err,
+                              hipStream_t stream) {
+  int m;
+  if (mode == DCUT_RS_SCAN) m = SEL_SCAN;
+  else if (mode == DCUT_RS_FIXED) m = SEL_FIXED;
+  else return DCUT_EINVAL;
+  return select_run(B, D, conf, draft, ctx_len, 1, m, R, budgets, costs, keep_len, cu, packed_tok,
+                    packed_pos, packed_req, choice, benefit, dev_err, stream);
 }

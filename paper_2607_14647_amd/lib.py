@@ -19,11 +19,13 @@ LIB_PATH = os.path.join(_PKG, "libdcut.so")
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
 DERR_CONF, DERR_TOKEN, DERR_CAPACITY = 1, 2, 4
 KERNELS = dict(NONE=0, SELECT=1, PACK=2, NORM=3, GEMM_QKV=4, ATTN=5, ATTN_COMBINE=6, GEMM_O=7,
-               GEMM_GATE_UP=8, GEMM_DOWN=9, MOE=10, LM_HEAD=11, ARGMAX_FINAL=12, ACCEPT=13)
+               GEMM_GATE_UP=8, GEMM_DOWN=9, MOE=10, LM_HEAD=11, ARGMAX_FINAL=12, ACCEPT=13,
+               RS_DECIDE=14, RS_RESIDUAL=15, RS_FINISH=16)
+RS_SCAN, RS_FIXED = 0, 1
 
 EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",
-           "dcut_lm_head_sample", "dcut_workspace_bytes", "dcut_strerror", "dcut_budgets_from_ratios",
-           "dcut_nearest_batch", "dcut_profile_arm"]
+           "dcut_lm_head_sample", "dcut_select_rs", "dcut_accept_rs", "dcut_workspace_bytes", "dcut_strerror",
+           "dcut_budgets_from_ratios", "dcut_nearest_batch", "dcut_profile_arm"]
 
 
 class DcutError(RuntimeError):
@@ -61,8 +63,11 @@ def _load() -> C.CDLL:
                                       vp, vp, C.POINTER(KV), vp, vp, vp, sz, vp]
     lib.dcut_lm_head_argmax.argtypes = [i32, i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp, sz, vp]
     lib.dcut_lm_head_sample.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, C.c_float, vp, C.c_float,
-                                        C.c_uint64, vp, vp, vp, sz, vp]
+                                        C.c_uint64, vp, vp, vp, vp, vp, sz, vp]
     lib.dcut_accept.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.dcut_select_rs.argtypes = [i32, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.dcut_accept_rs.argtypes = [i32, i32, i32, C.c_float, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   vp, vp, vp, vp, sz, vp, vp]
     lib.dcut_workspace_bytes.argtypes = [i32, C.POINTER(LayerCfg), i32, i32]
     lib.dcut_workspace_bytes.restype = sz
     lib.dcut_strerror.argtypes = [i32]
@@ -71,7 +76,8 @@ def _load() -> C.CDLL:
     lib.dcut_nearest_batch.argtypes = [i32, i32, vp]
     lib.dcut_profile_arm.argtypes = [i32, vp, vp]
     for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_sample", "dcut_accept",
-              "dcut_budgets_from_ratios", "dcut_nearest_batch", "dcut_profile_arm"]:
+              "dcut_select_rs", "dcut_accept_rs", "dcut_budgets_from_ratios", "dcut_nearest_batch",
+              "dcut_profile_arm"]:
         getattr(lib, f).restype = i32
     return lib
 
@@ -135,7 +141,7 @@ def profile_arm(kernel: str, start=None, stop=None) -> None:
     _check(_lib.dcut_profile_arm(kid, s, e), "dcut_profile_arm")
 
 
-# ------------------------------------------------------------------ the four calls
+# ------------------------------------------------------------------ the calls
 
 def select(B: int, D: int, conf: torch.Tensor, draft: torch.Tensor, ctx_len: torch.Tensor,
            budgets: Sequence[int], costs: Sequence[float], out: Dict[str, torch.Tensor],
@@ -148,6 +154,19 @@ def select(B: int, D: int, conf: torch.Tensor, draft: torch.Tensor, ctx_len: tor
                           _p(out["packed_tok"]), _p(out["packed_pos"]), _p(out["packed_req"]),
                           _p(out["choice"]), _p(out.get("benefit")), _p(dev_err), _stream(stream))
     _check(st, "dcut_select")
+
+
+def select_rs(B: int, D: int, conf: torch.Tensor, draft: torch.Tensor, ctx_len: torch.Tensor, mode: int,
+              budgets: Sequence[int], costs: Sequence[float], out: Dict[str, torch.Tensor],
+              dev_err: Optional[torch.Tensor] = None, stream=None) -> None:
+    R = len(budgets)
+    b = (C.c_int32 * max(R, 1))(*[int(x) for x in budgets])
+    c = (C.c_double * max(R, 1))(*[float(x) for x in costs])
+    st = _lib.dcut_select_rs(B, D, _p(conf), _p(draft), _p(ctx_len), int(mode), R, C.cast(b, C.c_void_p),
+                             C.cast(c, C.c_void_p), _p(out["keep_len"]), _p(out["cu"]),
+                             _p(out["packed_tok"]), _p(out["packed_pos"]), _p(out["packed_req"]),
+                             _p(out["choice"]), _p(out.get("benefit")), _p(dev_err), _stream(stream))
+    _check(st, "dcut_select_rs")
 
 
 def select_outputs(B: int, D: int, R: int, device="cuda") -> Dict[str, torch.Tensor]:
@@ -191,11 +210,12 @@ def lm_head_argmax(H: int, V: int, B: int, D: int, cu: torch.Tensor, x: torch.Te
 def lm_head_sample(H: int, V: int, B: int, D: int, cu: torch.Tensor, packed_req: torch.Tensor,
                    packed_pos: torch.Tensor, x: torch.Tensor, final_norm: torch.Tensor, eps: float,
                    w_lm: torch.Tensor, temperature: float, seed: int, token: torch.Tensor, ws: torch.Tensor,
-                   max_score: Optional[torch.Tensor] = None, stream=None) -> None:
+                   max_score: Optional[torch.Tensor] = None, logits: Optional[torch.Tensor] = None,
+                   lse: Optional[torch.Tensor] = None, stream=None) -> None:
     st = _lib.dcut_lm_head_sample(H, V, B, D, _p(cu), _p(packed_req), _p(packed_pos), _p(x), _p(final_norm),
                                   float(eps), _p(w_lm), float(temperature), int(seed) & 0xFFFFFFFFFFFFFFFF,
-                                  _p(token), _p(max_score), _p(ws), ws.numel() * ws.element_size(),
-                                  _stream(stream))
+                                  _p(token), _p(max_score), _p(logits), _p(lse), _p(ws),
+                                  ws.numel() * ws.element_size(), _stream(stream))
     _check(st, "dcut_lm_head_sample")
 
 
@@ -205,6 +225,18 @@ def accept(B: int, D: int, draft: torch.Tensor, keep_len: torch.Tensor, cu: torc
     st = _lib.dcut_accept(B, D, _p(draft), _p(keep_len), _p(cu), _p(argmax), _p(accept_len),
                           _p(next_tok), _p(total), _p(ctx_len_inout), _stream(stream))
     _check(st, "dcut_accept")
+
+
+def accept_rs(B: int, D: int, V: int, temperature: float, seed: int, draft: torch.Tensor, q: torch.Tensor,
+              keep_len: torch.Tensor, cu: torch.Tensor, packed_pos: torch.Tensor, logits: torch.Tensor,
+              lse: torch.Tensor, token: torch.Tensor, accept_len: torch.Tensor, next_tok: torch.Tensor,
+              total: torch.Tensor, ws: torch.Tensor, ctx_len_inout: Optional[torch.Tensor] = None,
+              dev_err: Optional[torch.Tensor] = None, stream=None) -> None:
+    st = _lib.dcut_accept_rs(B, D, V, float(temperature), int(seed) & 0xFFFFFFFFFFFFFFFF, _p(draft), _p(q),
+                             _p(keep_len), _p(cu), _p(packed_pos), _p(logits), _p(lse), _p(token),
+                             _p(accept_len), _p(next_tok), _p(total), _p(ctx_len_inout), _p(ws),
+                             ws.numel() * ws.element_size(), _p(dev_err), _stream(stream))
+    _check(st, "dcut_accept_rs")
 
 
 def workspace(nbytes: int, device="cuda") -> torch.Tensor:

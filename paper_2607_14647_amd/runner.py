@@ -51,13 +51,31 @@ class VerifyStep:
         self.ws_lm = L.workspace(L.workspace_bytes(2, self.lcfg, self.B, self.D), device)
         self.temperature = 0.0      # > 0: temperature sampling instead of the greedy argmax
         self.seed = 0
+        self.q = None               # proposal distributions [B][D][V]: rejection-sampling verification
+
+    def enable_rs(self, q) -> None:
+        """Switch to rejection-sampling verification with proposal distributions q [B][D][V]
+        (numpy or device tensor): the LM head then also writes logits and log-partition values."""
+        V = self.ly.vocab
+        self.q = q if isinstance(q, torch.Tensor) else _dev(np.asarray(q, dtype=np.float32), self.device)
+        assert tuple(self.q.shape) == (self.B, self.D, V) and self.q.dtype == torch.float32
+        self.logits = torch.empty(self.rows, V, dtype=torch.float32, device=self.device)
+        self.lse = torch.empty(self.rows, dtype=torch.float32, device=self.device)
+        self.ws_rs = L.workspace(L.workspace_bytes(4, self.lcfg, self.B, self.D), self.device)
 
     def set_draft(self, draft: np.ndarray) -> None:
         self.draft.copy_(torch.from_numpy(np.ascontiguousarray(draft, dtype=np.int32)))
 
+    def set_conf(self, conf: np.ndarray) -> None:
+        self.conf.copy_(torch.from_numpy(np.ascontiguousarray(conf, dtype=np.float32)))
+
     def select(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
         L.select(self.B, self.D, self.conf, self.draft, self.ctx_len, budgets, costs, self.sel,
                  self.dev_err)
+
+    def select_rs(self, mode: int, budgets: Sequence[int], costs: Sequence[float]) -> None:
+        L.select_rs(self.B, self.D, self.conf, self.draft, self.ctx_len, mode, budgets, costs, self.sel,
+                    self.dev_err)
 
     def verify(self, x_in: Optional[torch.Tensor] = None) -> None:
         L.verify_layer(self.lcfg, self.lw, self.B, self.D, self.sel, self.ctx_len, self.kvd, self.x,
@@ -70,7 +88,9 @@ class VerifyStep:
             L.lm_head_sample(self.ly.hidden, self.ly.vocab, self.B, self.D, self.sel["cu"],
                              self.sel["packed_req"], self.sel["packed_pos"], self.x, self.w["final_norm"],
                              self.ly.rms_eps, self.w["w_lm"], self.temperature, self.seed, self.argmax,
-                             self.ws_lm, max_score=self.max_logit)
+                             self.ws_lm, max_score=self.max_logit,
+                             logits=self.logits if self.q is not None else logits,
+                             lse=self.lse if self.q is not None else None)
             return
         L.lm_head_argmax(self.ly.hidden, self.ly.vocab, self.B, self.D, self.sel["cu"], self.x,
                          self.w["final_norm"], self.ly.rms_eps, self.w["w_lm"], self.argmax,
@@ -79,6 +99,12 @@ class VerifyStep:
     def accept(self, ctx_inout: Optional[torch.Tensor] = None) -> None:
         L.accept(self.B, self.D, self.draft, self.sel["keep_len"], self.sel["cu"], self.argmax,
                  self.accept_len, self.next_tok, self.total, ctx_inout)
+
+    def accept_rs(self, ctx_inout: Optional[torch.Tensor] = None) -> None:
+        L.accept_rs(self.B, self.D, self.ly.vocab, self.temperature, self.seed, self.draft, self.q,
+                    self.sel["keep_len"], self.sel["cu"], self.sel["packed_pos"], self.logits, self.lse,
+                    self.argmax, self.accept_len, self.next_tok, self.total, self.ws_rs, ctx_inout,
+                    self.dev_err)
 
     def step(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
         self.select(budgets, costs)

@@ -30,6 +30,7 @@ BF16_ONE = np.uint16(0x3F80)
 
 _TAGS = {
     "conf": 1, "draft": 2, "ctx": 3, "match": 4, "amix": 5, "perm": 6,
+    "q": 7, "q_draw": 8, "q_beta": 9,
     "embed": 10, "w_qkv": 11, "w_o": 12, "w_gate_up": 13, "w_down": 14,
     "w_lm": 15, "w_router": 16, "w_exp_gate_up": 17, "w_exp_down": 18,
     "kv_k": 20, "kv_v": 21, "argmax": 30,
@@ -259,3 +260,31 @@ def synthetic_argmax(cfg: Config, seed: int, draft: np.ndarray, match_u: np.ndar
     hit = match_u < conf
     g[:, :D] = np.where(hit, draft[:, 1:], g[:, :D])
     return g
+
+
+def make_proposals(cfg: Config, seed: int, bonus: np.ndarray) -> Dict[str, np.ndarray]:
+    """Proposal distributions of a stochastic drafter, for rejection-sampling tests.
+
+    q[i][k-1] = softmax(beta_i * g) over the vocabulary with g ~ N(0, 1) per
+    entry and beta_i ~ U[1, 4] per request (larger beta, more peaked), formed in
+    float64 and stored as float32.  Draft z_{i,k} is drawn from q[i][k-1] by
+    inverse CDF with its own stored uniform, and its confidence is
+    q[i][k-1][z_{i,k}] (the drafter's probability of what it proposed).
+    Column 0 of `draft` is `bonus`."""
+    B, D, V = cfg.B, cfg.D, cfg.layer.vocab
+    beta = _gen(seed, cfg.cid, "q_beta").uniform(1.0, 4.0, size=B)
+    q = np.empty((B, D, V), dtype=np.float32)
+    draft = np.zeros((B, D + 1), dtype=np.int32)
+    draft[:, 0] = np.asarray(bonus, dtype=np.int32)
+    conf = np.zeros((B, D), dtype=np.float32)
+    for i in range(B):
+        gi = _gen(seed, cfg.cid, "q", i).standard_normal((D, V)) * beta[i]
+        e = np.exp(gi - gi.max(axis=1, keepdims=True))
+        qi = (e / e.sum(axis=1, keepdims=True)).astype(np.float32)
+        q[i] = qi
+        u = _gen(seed, cfg.cid, "q_draw", i).random(D)
+        cdf = np.cumsum(qi.astype(np.float64), axis=1)
+        z = np.minimum((cdf < (u * cdf[:, -1])[:, None]).sum(axis=1), V - 1)
+        draft[i, 1:] = z
+        conf[i] = qi[np.arange(D), z]
+    return dict(q=q, draft=draft, conf=conf, beta=beta)

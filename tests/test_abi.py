@@ -64,6 +64,10 @@ def test_workspace_sizes():
     assert 0 < ws1 < (1 << 31) and ws1 % 256 == 0
     # normalised rows plus up to one key per row and 64 columns of the vocabulary
     assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 1024 * 2 * ((cfg.vocab + 127) // 128) * 8
+    # RS acceptance: two int32 per request plus one key per request and 2048-column chunk
+    nch = (cfg.vocab + 2047) // 2048
+    assert L.workspace_bytes(4, cfg, 64, 15) >= 64 * 8 + 64 * nch * 8
+    assert L.workspace_bytes(4, None, 64, 15) == 2 ** 64 - 1
     assert L.workspace_bytes(1, cfg, 0, 15) == 2 ** 64 - 1
     bad = L.LayerCfg(4096, 32, 7, 128, 14336, 0, 0, 0, 128256, 4112, 1e-5, 5e5)
     assert L.workspace_bytes(1, bad, 64, 15) == 2 ** 64 - 1
@@ -90,6 +94,24 @@ def test_select_rejects_invalid_args(B, D, R, budgets, costs):
     assert _sel_call(B, D, R, budgets, costs) == L.EINVAL
 
 
+def _sel_rs_call(mode, R, budgets, costs):
+    lib = L.lib()
+    b = (C.c_int32 * max(R, 1))(*budgets)
+    c = (C.c_double * max(R, 1))(*costs)
+    fake = C.c_void_p(0x1000)
+    return lib.dcut_select_rs(4, 15, fake, fake, fake, mode, R, C.cast(b, C.c_void_p), C.cast(c, C.c_void_p),
+                              fake, fake, fake, fake, fake, fake, None, None, None)
+
+
+def test_select_rs_rejects_invalid_args():
+    assert _sel_rs_call(2, 1, [8], [1.0]) == L.EINVAL                      # unknown mode
+    assert _sel_rs_call(-1, 1, [8], [1.0]) == L.EINVAL
+    assert _sel_rs_call(L.RS_FIXED, 2, [8, 16], [1.0, 2.0]) == L.EINVAL    # a fixed budget is one budget
+    assert _sel_rs_call(L.RS_SCAN, 1, [3], [1.0]) == L.EINVAL              # below B
+    assert _sel_rs_call(L.RS_SCAN, 2, [16, 8], [1.0, 2.0]) == L.EINVAL     # decreasing
+    assert _sel_rs_call(L.RS_SCAN, 1, [8], [0.0]) == L.EINVAL
+
+
 def test_select_rejects_null_outputs():
     assert _sel_call(4, 15, 1, [8], [1.0], null_out=True) == L.EINVAL
 
@@ -104,8 +126,8 @@ def test_other_entry_points_reject_invalid_args():
     assert lib.dcut_lm_head_argmax(4096, 10, 4, 15, fake, fake, fake, 1e-5, fake, fake, None, None,
                                    None, 0, None) == L.EWORKSPACE
     # temperature sampling: null request/position arrays, non-positive or infinite temperature
-    smp = lambda req, pos, T, wsb: lib.dcut_lm_head_sample(4096, 10, 4, 15, fake, req, pos, fake, fake, 1e-5,
-                                                           fake, T, 7, fake, None, fake, wsb, None)
+    smp = lambda req, pos, T, wsb, lg=None, lse=None: lib.dcut_lm_head_sample(
+        4096, 10, 4, 15, fake, req, pos, fake, fake, 1e-5, fake, T, 7, fake, None, lg, lse, fake, wsb, None)
     assert smp(None, fake, 1.0, 1 << 30) == L.EINVAL
     assert smp(fake, None, 1.0, 1 << 30) == L.EINVAL
     assert smp(fake, fake, 0.0, 1 << 30) == L.EINVAL
@@ -113,6 +135,7 @@ def test_other_entry_points_reject_invalid_args():
     assert smp(fake, fake, float("inf"), 1 << 30) == L.EINVAL
     assert smp(fake, fake, float("nan"), 1 << 30) == L.EINVAL
     assert smp(fake, fake, 1.0, 0) == L.EWORKSPACE
+    assert smp(fake, fake, 1.0, 1 << 30, lg=None, lse=fake) == L.EINVAL      # lse needs the logits
     cfg = L.LayerCfg(256, 4, 2, 64, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
     w = L.LayerW(*([0x1000] * 7 + [None] * 3))
     kv = L.KV(0x1000, 0x1000, 0x1000, 0x1000)
@@ -123,6 +146,15 @@ def test_other_entry_points_reject_invalid_args():
     assert args(bad, 1 << 30) == L.EINVAL
     hd = L.LayerCfg(256, 4, 2, 96, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
     assert args(hd, 1 << 30) == L.EUNSUPPORTED
+    # RS acceptance: sizes, temperature, null pointers, then the workspace
+    acc = lambda B, V, T, q, wsb: lib.dcut_accept_rs(B, 15, V, T, 3, fake, q, fake, fake, fake, fake, fake, fake,
+                                                      fake, fake, fake, None, fake, wsb, None, None)
+    assert acc(0, 10, 1.0, fake, 1 << 30) == L.EINVAL
+    assert acc(4, 0, 1.0, fake, 1 << 30) == L.EINVAL
+    assert acc(4, 10, 0.0, fake, 1 << 30) == L.EINVAL
+    assert acc(4, 10, float("inf"), fake, 1 << 30) == L.EINVAL
+    assert acc(4, 10, 1.0, None, 1 << 30) == L.EINVAL
+    assert acc(4, 10, 1.0, fake, 0) == L.EWORKSPACE
     assert lib.dcut_profile_arm(99, None, None) == L.EINVAL
     assert lib.dcut_profile_arm(L.KERNELS["LM_HEAD"], None, None) == L.EINVAL
     assert lib.dcut_profile_arm(0, None, None) == L.OK
