@@ -18,6 +18,10 @@ Sequence:
      with the dominant kernel timed by HIP events inside the same region;
   6. CPU baseline: the oracle on a bounded sample of the same batch.
 Prints one JSON line.
+
+`--temperature T` samples the target's tokens (dcut_lm_head_sample); `--rs`
+verifies by rejection sampling (dcut_select_rs, dcut_lm_head_sample with
+logits, dcut_accept_rs) against a synthetic stochastic drafter.
 """
 import argparse
 import hashlib
@@ -160,6 +164,10 @@ def main():
                          "dcut_lm_head_sample (the paper's temperature-1 regime); drafts are forced from "
                          "the same sampled tokens")
     ap.add_argument("--sample-seed", type=int, default=1, help="seed of the sampling noise")
+    ap.add_argument("--rs", action="store_true",
+                    help="rejection-sampling verification (dcut_select_rs with the causal scan, "
+                         "dcut_lm_head_sample with logits, dcut_accept_rs) against a synthetic stochastic "
+                         "drafter; temperature 1 unless --temperature is given")
     ap.add_argument("--state", default=None,
                     help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
                          "run of the same workload; written when missing, reused when present (a "
@@ -178,6 +186,8 @@ def main():
     from paper_2607_14647_amd import workload as wl
 
     assert torch.cuda.is_available(), "bench.py needs an MI355X GPU"
+    if args.rs and args.temperature == 0:
+        args.temperature = 1.0
     cfg = wl.CONFIGS[args.config]
     ly = cfg.layer
     log(f"workload cfg{cfg.cid} ({cfg.name}) seed {args.seed}: generating")
@@ -195,6 +205,12 @@ def main():
         state = json.load(open(args.state))
         assert state["workload"] == [cfg.cid, args.seed] and state["budgets"] == budgets, "state mismatch"
         assert state.get("temperature", 0.0) == args.temperature, "state mismatch (temperature)"
+        assert state.get("rs", False) == args.rs, "state mismatch (rs)"
+    if args.rs:
+        vs.enable_rs(None)
+        log("stochastic drafter: proposals and drafts from the target's own distributions (D passes)")
+        runner.force_drafts_rs_on_device(vs, st["draft"], st["conf"], st["match_u"], args.sample_seed + 1000)
+    elif state is not None:
         vs.set_draft(np.array(state["draft"], dtype=np.int32))
         log(f"reusing forced drafts, cost row and dominant kernel from {args.state}")
     else:
@@ -221,17 +237,19 @@ def main():
         cost_ms, acc_per_k = state["cost_row_ms"], state["accepted_per_budget"]
     else:
         log("cost row: every candidate budget alone")
+    run_step = vs.step_rs if args.rs else vs.step
     for K in (budgets if state is None else []):
-        step = lambda K=K: vs.step([K], [1.0])
+        step = lambda K=K: run_step([K], [1.0])
         timed(step, 2)
         cost_ms.append(statistics.median(timed(step, args.cost_reps)))
         acc_per_k.append(int(vs.total.item()))
     log("cost row (ms): " + ", ".join(f"{K}:{c:.3f}" for K, c in zip(budgets, cost_ms)))
-    adaptive = lambda: vs.step(budgets, cost_ms)
+    adaptive = lambda: run_step(budgets, cost_ms)
 
     # 4. per-kernel breakdown with the timing hook
     names = ["SELECT", "PACK", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP",
-             "GEMM_DOWN", "LM_HEAD", "ARGMAX_FINAL", "ACCEPT"]
+             "GEMM_DOWN", "LM_HEAD", "ARGMAX_FINAL"]
+    names += ["RS_DECIDE", "RS_RESIDUAL", "RS_FINISH"] if args.rs else ["ACCEPT"]
     breakdown = {} if state is None else state["kernel_us"]
     for nm in (names if state is None else []):
         pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
@@ -248,6 +266,7 @@ def main():
     dominant = max(breakdown, key=lambda k: breakdown[k])
     if args.state and state is None:
         json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,
+                       rs=args.rs,
                        accepted_per_budget=acc_per_k, kernel_us=breakdown,
                        draft=vs.host("draft").tolist()), open(args.state, "w"))
     log("kernel us: " + ", ".join(f"{k}={v}" for k, v in breakdown.items()) + f"; dominant {dominant}")
@@ -316,7 +335,9 @@ def main():
                     global_batch=cfg.B, K_star=Kstar, r_star=rstar, accepted_per_step=accepted,
                     budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm",
                     target_decoding="greedy" if args.temperature == 0 else
-                    f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})"),
+                    (f"rejection sampling at temperature {args.temperature} (causal scan over shifted "
+                     f"scores; seed {args.sample_seed})" if args.rs else
+                     f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})")),
         hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         step_algorithmic_bytes=int(step_bytes),
         roofline=rl,

@@ -132,8 +132,9 @@ int dcut_select(int B, int D, const float *conf, const int32_t *draft, const int
  *     DCUT_RS_FIXED  a budget fixed before the block was drafted (for example
  *                    from earlier steps' statistics): R must be 1 and K* = K_0,
  *                    the global top-K_0 of the shifted scores; choice = {K_0, 0}.
- * The proposals' conditional distributions q must be the ones the
- * confidences come from: c_{i,k} = q_{i,k}(z_{i,k}).
+ * The paper takes c_{i,k} = q_{i,k}(z_{i,k}), the drafter's probability of its
+ * own proposal; causality needs only that c_{i,k} depend on no proposal after
+ * z_{i,k}.
  *
  *   mode      DCUT_RS_SCAN or DCUT_RS_FIXED
  *   every other argument as for dcut_select (benefit[r] sums shifted scores)
@@ -253,13 +254,12 @@ int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const flo
  *   token     dev [B(D+1)] int32 out;   max_score dev [B(D+1)] float32 out (nullable):
  *             the winning logits / T + G
  *   logits    dev [B(D+1)][V] float32 out (nullable): the raw logits of rows < K*
- *   lse       dev [B(D+1)] float32 out (nullable; needs logits):
- *             ln sum_c exp(logits[t][c] * (1/T)), the row's log-partition
- *             function (dcut_accept_rs takes logits and lse)
+ *   lse       dev [B(D+1)] float32 out (nullable): ln sum_c exp(logits[t][c] * (1/T)),
+ *             the row's log-partition function, from the GEMM's float32
+ *             accumulators (dcut_accept_rs takes logits and lse)
  *   other arguments and the workspace as for dcut_lm_head_argmax
- * Errors: DCUT_EINVAL for a null request/position array, a temperature that
- * is not positive and finite, or lse without logits; otherwise as
- * dcut_lm_head_argmax.
+ * Errors: DCUT_EINVAL for a null request/position array or a temperature that
+ * is not positive and finite, otherwise as dcut_lm_head_argmax.
  */
 int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu, const int32_t *packed_req,
                         const int32_t *packed_pos, const float *x, const dcut_bf16 *final_norm,

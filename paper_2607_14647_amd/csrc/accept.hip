@@ -71,8 +71,9 @@ extern "C" int dcut_accept(int B, int D, const int32_t *draft, const int32_t *ke
 // uniform of the row.  At the first rejection the committed token is drawn
 // from (p_r - q_{i,j})_+ by the Gumbel-max rule with the row's own noise; when
 // every kept draft is accepted it is the target's sample at the last kept row.
-// Three launches: the per-request decisions, the residual draws over the
-// vocabulary (one workgroup per request and column chunk), and the merge.
+// Three launches: the decisions (one workgroup, every kept draft tested at
+// once), the residual draws over the vocabulary (one workgroup per request and
+// column chunk), and the merge.
 namespace dcut {
 
 constexpr int RS_CHUNK = 2048;     // vocabulary columns per residual workgroup
@@ -93,40 +94,50 @@ __device__ __forceinline__ void block_bounds(int i, int B, int D, const int32_t 
   base = base < 0 ? 0 : (base > rows - 1 - n ? rows - 1 - n : base);   // stay in bounds
 }
 
-// One thread per request: walk the kept drafts in order until one is rejected.
-__global__ void __launch_bounds__(256)
+// Every (request, depth) test at once; the first failing depth of each request
+// (an LDS minimum) is where its verification stops.
+__global__ void __launch_bounds__(1024)
 k_rs_decide(int B, int D, int V, float inv_temp, uint32_t seed_lo, uint32_t seed_hi,
             const int32_t *__restrict__ draft, const float *__restrict__ q,
             const int32_t *__restrict__ keep_len, const int32_t *__restrict__ cu,
             const int32_t *__restrict__ packed_pos, const float *__restrict__ logits,
             const float *__restrict__ lse, int32_t *__restrict__ rej_row, int32_t *__restrict__ acc,
             int32_t *__restrict__ dev_err) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= B) return;
-  int n, base;
-  block_bounds(i, B, D, keep_len, cu, n, base);
-  int a = 0;
-  bool rej = false;
-  for (int j = 1; j <= n; ++j) {
-    const int r = base + j - 1;
-    const int z = draft[(size_t)i * (D + 1) + j];
-    if (z < 0 || z >= V) {               // an invalid draft is never accepted
-      if (dev_err) atomicOr(dev_err, DCUT_DERR_TOKEN);
-      rej = true;
-      break;
-    }
-    const double p = exp((double)(logits[(size_t)r * V + z] * inv_temp) - (double)lse[r]);
-    const double qz = (double)q[((size_t)i * D + (j - 1)) * V + z];
-    const uint4 w = philox4x32_10(make_uint4(0u, (uint32_t)packed_pos[r], (uint32_t)i, 1u), seed_lo, seed_hi);
-    if (uniform01(w.x) * qz < p) {
-      ++a;
-    } else {
-      rej = true;
-      break;
-    }
+  __shared__ int s_n[DCUT_MAX_BATCH], s_base[DCUT_MAX_BATCH], s_first[DCUT_MAX_BATCH];
+  __shared__ int s_err;
+  if (threadIdx.x == 0) s_err = 0;
+  for (int i = threadIdx.x; i < B; i += blockDim.x) {
+    int n, base;
+    block_bounds(i, B, D, keep_len, cu, n, base);
+    s_n[i] = n;
+    s_base[i] = base;
+    s_first[i] = n;                    // no failure among the n kept drafts
   }
-  rej_row[i] = rej ? base + a : -1;
-  acc[i] = a;
+  __syncthreads();
+  // draft j = d + 1 of request i is tested at row base + d
+  for (int idx = threadIdx.x; idx < B * D; idx += blockDim.x) {
+    const int i = idx / D, d = idx - i * D;
+    if (d >= s_n[i]) continue;
+    const int r = s_base[i] + d;
+    const int z = draft[(size_t)i * (D + 1) + d + 1];
+    bool pass = false;
+    if (z < 0 || z >= V) {               // an invalid draft is never accepted
+      s_err = 1;
+    } else {
+      const double p = exp((double)(logits[(size_t)r * V + z] * inv_temp) - (double)lse[r]);
+      const double qz = (double)q[((size_t)i * D + d) * V + z];
+      const uint4 w = philox4x32_10(make_uint4(0u, (uint32_t)packed_pos[r], (uint32_t)i, 1u), seed_lo, seed_hi);
+      pass = uniform01(w.x) * qz < p;
+    }
+    if (!pass) atomicMin(&s_first[i], d);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < B; i += blockDim.x) {
+    const int a = s_first[i];
+    rej_row[i] = a < s_n[i] ? s_base[i] + a : -1;
+    acc[i] = a;
+  }
+  if (threadIdx.x == 0 && s_err && dev_err) atomicOr(dev_err, DCUT_DERR_TOKEN);
 }
 
 // Residual draw of a rejecting row over one chunk of the vocabulary: the
@@ -182,7 +193,8 @@ k_rs_residual(int D, int V, int nch, float inv_temp, uint32_t seed_lo, uint32_t 
   }
 }
 
-// Committed token, accepted length and totals.
+// Committed token, accepted length and totals: one wave per request merges
+// the residual keys of its chunks.
 __global__ void __launch_bounds__(1024)
 k_rs_finish(int B, int D, int nch, const int32_t *__restrict__ keep_len, const int32_t *__restrict__ cu,
             const int32_t *__restrict__ token, const int32_t *__restrict__ rej_row,
@@ -190,26 +202,32 @@ k_rs_finish(int B, int D, int nch, const int32_t *__restrict__ keep_len, const i
             int32_t *__restrict__ accept_len, int32_t *__restrict__ next_tok, int32_t *__restrict__ total,
             int32_t *__restrict__ ctx_len_inout) {
   __shared__ int s_wave[17];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int local = 0;
-  for (int i = threadIdx.x; i < B; i += blockDim.x) {
-    int n, base;
-    block_bounds(i, B, D, keep_len, cu, n, base);
+  for (int i = wv; i < B; i += nw) {
     const int a = acc[i], r = rej_row[i];
-    int t;
-    if (r >= 0) {
-      unsigned long long k = 0ull;
-      for (int c = 0; c < nch; ++c) {
+    unsigned long long k = 0ull;
+    if (r >= 0)
+      for (int c = lane; c < nch; c += 64) {
         const unsigned long long v = keys[(size_t)i * nch + c];
         k = v > k ? v : k;
       }
-      t = k ? (int32_t)(0xffffffffu - (uint32_t)(k & 0xffffffffu)) : token[r];   // empty residual: p itself
-    } else {
-      t = token[base + a];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const unsigned long long o = __shfl_xor(k, off, 64);
+      k = o > k ? o : k;
     }
-    accept_len[i] = a;
-    next_tok[i] = t;
-    local += a + 1;
-    if (ctx_len_inout) ctx_len_inout[i] += a + 1;
+    if (lane == 0) {
+      int n, base;
+      block_bounds(i, B, D, keep_len, cu, n, base);
+      int t;
+      if (r >= 0) t = k ? (int32_t)(0xffffffffu - (uint32_t)(k & 0xffffffffu)) : token[r];   // empty residual: p
+      else t = token[base + a];
+      accept_len[i] = a;
+      next_tok[i] = t;
+      local += a + 1;
+      if (ctx_len_inout) ctx_len_inout[i] += a + 1;
+    }
   }
   int sum;
   block_exclusive_scan(local, s_wave, &sum);
@@ -237,7 +255,7 @@ extern "C" int dcut_accept_rs(int B, int D, int V, float temperature, uint64_t s
   unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)B * 2 * sizeof(int32_t)));
   const float inv_temp = 1.0f / temperature;
   const uint32_t lo = (uint32_t)seed, hi = (uint32_t)(seed >> 32);
-  DCUT_TRY(launch(DCUT_KERNEL_RS_DECIDE, k_rs_decide, dim3((B + 255) / 256), dim3(256), 0, stream, B, D, V,
+  DCUT_TRY(launch(DCUT_KERNEL_RS_DECIDE, k_rs_decide, dim3(1), dim3(1024), 0, stream, B, D, V,
                   inv_temp, lo, hi, draft, q, keep_len, cu, packed_pos, logits, lse, rej_row, acc, dev_err));
   if (D > 0)
     DCUT_TRY(launch(DCUT_KERNEL_RS_RESIDUAL, k_rs_residual, dim3(nch, B), dim3(256), 0, stream, D, V, nch,

@@ -107,6 +107,8 @@ struct GemmArgs {
   float inv_temp;
   uint32_t seed_lo, seed_hi;
   const int32_t *row_req, *row_pos;
+  float2 *lse_part;               // EPI_SAMPLE, optional [M_max][amax_slots]: per column range
+                                  // (max x, sum exp(x - max)) of x = acc * inv_temp
   float *logits;                  // optional [M][N] float32
   long long ld_logits;
   // split-K (EPI_RESID_F32 / EPI_STORE_F32): partial tiles [splits][M_max][N] float32

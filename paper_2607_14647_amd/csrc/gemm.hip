@@ -472,6 +472,48 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
         }
         __builtin_amdgcn_wave_barrier();
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if constexpr (EPI == EPI_SAMPLE) {
+          // the row's log-partition partials over the same column range: each
+          // lane's (max, rescaled sum) over its WN columns, merged per row
+          // through the same LDS transpose
+          if (a.lse_part) {
+            float2 *kf = (float2 *)kl;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              float x[WN];
+              float m = -__builtin_inff();
+#pragma unroll
+              for (int j = 0; j < WN; ++j) {
+                x[j] = col0 + 32 * j < a.N ? acc[i][j][r] * a.inv_temp : -__builtin_inff();
+                m = fmaxf(m, x[j]);
+              }
+              float sum = 0.0f;
+#pragma unroll
+              for (int j = 0; j < WN; ++j) sum += __expf(x[j] - m);
+              if (m == -__builtin_inff()) sum = 0.0f;
+              kf[(8 * (r >> 2) + 4 * kh + (r & 3)) * KS + l32] = make_float2(m, sum);
+            }
+            __builtin_amdgcn_wave_barrier();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            if (lane < 32) {
+              float m = -__builtin_inff();
+#pragma unroll 8
+              for (int c = 0; c < 32; ++c) m = fmaxf(m, kf[lane * KS + c].x);
+              float sum = 0.0f;
+              if (m != -__builtin_inff()) {
+#pragma unroll 8
+                for (int c = 0; c < 32; ++c) {
+                  const float2 v = kf[lane * KS + c];
+                  sum += v.y * __expf(v.x - m);
+                }
+              }
+              const int gm = m0 + wm * WM * 32 + i * 32 + lane;
+              if (gm < Mlim) a.lse_part[(size_t)gm * a.amax_slots + slot] = make_float2(m, sum);
+            }
+            __builtin_amdgcn_wave_barrier();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          }
+        }
       };
       static_assert(WM >= 1 && WM <= 4, "row blocks per wave");
       row_block(std::integral_constant<int, 0>{});

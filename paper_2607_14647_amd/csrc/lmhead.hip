@@ -16,14 +16,15 @@ namespace dcut {
 size_t lmhead_ws_bytes(int H, int V, int B, int D) {
   const size_t M = (size_t)B * (D + 1);
   const size_t slots = 2 * (((size_t)V + 127) / 128);   // row stride of the partial keys
-  return align256(M * H * 2) + align256(M * slots * sizeof(unsigned long long));
+  // normalised rows, partial keys, partial log-partition pairs
+  return align256(M * H * 2) + 2 * align256(M * slots * sizeof(unsigned long long));
 }
 
 namespace {
 
 // One workgroup per row: the maximum of the row's partial keys, decoded; with
-// `lse`, also ln sum_c exp(logits[c] * inv_temp) of the row's written logits
-// (an online maximum and rescaled sum per thread, merged across the group).
+// `lse`, also ln sum_c exp(logits[c] * inv_temp) merged from the row's
+// per-range (max, rescaled sum) pairs.
 __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2) {
   const float M = fmaxf(m, m2);
   if (M == -__builtin_inff()) return;      // both empty
@@ -32,10 +33,9 @@ __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2
 }
 
 __global__ void __launch_bounds__(256)
-k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int stride,
-               const int32_t *__restrict__ m_count, int M_max, int32_t *__restrict__ argmax,
-               float *__restrict__ max_logit, const float *__restrict__ logits, int V, float inv_temp,
-               float *__restrict__ lse) {
+k_argmax_final(const unsigned long long *__restrict__ keys, const float2 *__restrict__ part, int slots,
+               int stride, const int32_t *__restrict__ m_count, int M_max, int32_t *__restrict__ argmax,
+               float *__restrict__ max_logit, float *__restrict__ lse) {
   __shared__ unsigned long long s_max[4];
   __shared__ float s_m[4], s_s[4];
   const int t = blockIdx.x;
@@ -43,58 +43,42 @@ k_argmax_final(const unsigned long long *__restrict__ keys, int slots, int strid
   const int tid = threadIdx.x, lane = tid & 63;
   const unsigned long long *row = keys + (size_t)t * stride;
   unsigned long long k = 0ull;
+  float m = -__builtin_inff(), sum = 0.0f;
   for (int s = tid; s < slots; s += 256) {
     const unsigned long long v = row[s];
     k = v > k ? v : k;
+    if (lse) {
+      const float2 p = part[(size_t)t * stride + s];
+      lse_merge(m, sum, p.x, p.y);
+    }
   }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     const unsigned long long o = __shfl_xor(k, off, 64);
     k = o > k ? o : k;
-  }
-  if (lane == 0) s_max[tid >> 6] = k;
-  if (lse) {
-    float m = -__builtin_inff(), sum = 0.0f;
-    const float *lr = logits + (size_t)t * V;
-    auto add = [&](float x) {
-      x *= inv_temp;
-      const float M = fmaxf(m, x);
-      sum = sum * __expf(m - M) + __expf(x - M);
-      m = M;
-    };
-    if ((V & 3) == 0) {
-      const float4 *l4 = (const float4 *)lr;
-      for (int c = tid; c < (V >> 2); c += 256) {
-        const float4 v = l4[c];
-        add(v.x); add(v.y); add(v.z); add(v.w);
-      }
-    } else {
-      for (int c = tid; c < V; c += 256) add(lr[c]);
-    }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
+    if (lse) {
       const float m2 = __shfl_xor(m, off, 64), s2 = __shfl_xor(sum, off, 64);
       lse_merge(m, sum, m2, s2);
     }
-    if (lane == 0) {
-      s_m[tid >> 6] = m;
-      s_s[tid >> 6] = sum;
-    }
+  }
+  if (lane == 0) {
+    s_max[tid >> 6] = k;
+    s_m[tid >> 6] = m;
+    s_s[tid >> 6] = sum;
   }
   __syncthreads();
   if (tid != 0) return;
-  for (int w = 1; w < 4; ++w) k = s_max[w] > k ? s_max[w] : k;
+  for (int w = 1; w < 4; ++w) {
+    k = s_max[w] > k ? s_max[w] : k;
+    lse_merge(m, sum, s_m[w], s_s[w]);
+  }
   argmax[t] = (int32_t)(0xffffffffu - (uint32_t)(k & 0xffffffffu));
   if (max_logit) {
     uint32_t u = (uint32_t)(k >> 32);
     u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
     max_logit[t] = __uint_as_float(u);
   }
-  if (lse) {
-    float m = s_m[0], sum = s_s[0];
-    for (int w = 1; w < 4; ++w) lse_merge(m, sum, s_m[w], s_s[w]);
-    lse[t] = m + __logf(sum);
-  }
+  if (lse) lse[t] = m + __logf(sum);
 }
 
 }  // namespace
@@ -110,14 +94,14 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
                        float *logits, float *lse, void *ws, size_t ws_bytes, hipStream_t stream) {
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
   if (!cu || !x || !final_norm || !w_lm || !token || !(eps >= 0.0f)) return DCUT_EINVAL;
-  if (lse && !logits) return DCUT_EINVAL;
   const size_t need = lmhead_ws_bytes(H, V, B, D);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
   uint16_t *f = (uint16_t *)ws;
-  unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)M * H * 2));
-  const int32_t *Kstar = cu + B;
   const int slots = 2 * ((V + 127) / 128);   // row stride; the GEMM writes gemm_argmax_slots() of them
+  unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)M * H * 2));
+  float2 *part = (float2 *)((char *)keys + align256((size_t)M * slots * sizeof(unsigned long long)));
+  const int32_t *Kstar = cu + B;
   DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x, nullptr, nullptr, 0, final_norm, eps, H, M, Kstar,
                           nullptr, f, nullptr, 0, 0.0f, nullptr, nullptr, nullptr, stream));
   GemmArgs g = {};
@@ -125,12 +109,13 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   g.W = w_lm; g.ldw = H; g.N = V;
   g.amax_keys = keys; g.amax_slots = slots; g.logits = logits; g.ld_logits = V;
   g.row_req = row_req; g.row_pos = row_pos; g.inv_temp = inv_temp;
+  g.lse_part = lse ? part : nullptr;
   g.seed_lo = (uint32_t)seed; g.seed_hi = (uint32_t)(seed >> 32);
   const int used = gemm_argmax_slots(g);
   DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, epi, g, stream));
   return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3(M), dim3(256), 0, stream,
-                (const unsigned long long *)keys, used, slots, Kstar, M, token, max_score,
-                (const float *)logits, V, inv_temp, lse);
+                (const unsigned long long *)keys, (const float2 *)part, used, slots, Kstar, M, token,
+                max_score, lse);
 }
 
 extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,

@@ -1,4 +1,4 @@
-"""Device-resident verify step: uploads a workload once and runs the four calls.
+"""Device-resident verify step: uploads a workload once and runs the library calls.
 
 Holds every buffer the C ABI needs (weights, KV cache, step inputs, outputs,
 workspaces) as torch device tensors and calls the library on torch's current
@@ -55,8 +55,11 @@ class VerifyStep:
 
     def enable_rs(self, q) -> None:
         """Switch to rejection-sampling verification with proposal distributions q [B][D][V]
-        (numpy or device tensor): the LM head then also writes logits and log-partition values."""
+        (numpy or device tensor; None allocates zeros to fill later): the LM head then also
+        writes logits and log-partition values."""
         V = self.ly.vocab
+        if q is None:
+            q = torch.zeros(self.B, self.D, V, dtype=torch.float32, device=self.device)
         self.q = q if isinstance(q, torch.Tensor) else _dev(np.asarray(q, dtype=np.float32), self.device)
         assert tuple(self.q.shape) == (self.B, self.D, V) and self.q.dtype == torch.float32
         self.logits = torch.empty(self.rows, V, dtype=torch.float32, device=self.device)
@@ -112,6 +115,14 @@ class VerifyStep:
         self.lm_head()
         self.accept()
 
+    def step_rs(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
+        """One rejection-sampling step: the causal scan over the candidates, or
+        the fixed budget when only one is given."""
+        self.select_rs(L.RS_FIXED if len(budgets) == 1 else L.RS_SCAN, budgets, costs)
+        self.verify()
+        self.lm_head()
+        self.accept_rs()
+
     def host(self, name: str) -> np.ndarray:
         src = self.sel[name] if name in self.sel else getattr(self, name)
         return src.cpu().numpy()
@@ -136,4 +147,44 @@ def force_drafts_on_device(st: VerifyStep, draft: np.ndarray, conf: np.ndarray,
         hit = match_u[:, k - 1] < conf[:, k - 1]
         z[hit, k] = g[hit, k - 1]
     st.set_draft(z)
+    return z
+
+
+def force_drafts_rs_on_device(st: VerifyStep, draft: np.ndarray, conf: np.ndarray, match_u: np.ndarray,
+                              seed: int) -> np.ndarray:
+    """Synthetic stochastic drafter for benchmarks of rejection-sampling verification.
+
+    At depth k the proposal is q_{i,k} = c p + (1 - c) delta_w: the target's own
+    distribution p at block position k-1 (the verify step's logits at the
+    drafting seed's temperature), mixed with a point mass on an unrelated token
+    w = draft[i][k]; c = conf[i][k-1].  The draft is the target's own draw
+    at that row when match_u < c and w otherwise, a draw from q_{i,k}.  RS
+    then accepts it with probability about c, as the greedy drafter's drafts
+    survive with probability c.  Depth order, full budget each pass; the
+    proposals land in st.q (enable_rs first).  Returns the drafts."""
+    B, D, V = st.B, st.D, st.ly.vocab
+    z = np.array(draft, dtype=np.int32, copy=True)
+    full = [B * (D + 1)]
+    keep_seed = st.seed
+    st.seed = seed
+    rows = torch.arange(B, device=st.device) * (D + 1)
+    c = torch.from_numpy(np.ascontiguousarray(conf, dtype=np.float32)).to(st.device)
+    w = torch.from_numpy(np.ascontiguousarray(draft[:, 1:], dtype=np.int64)).to(st.device)
+    for k in range(1, D + 1):
+        st.set_draft(z)
+        st.select(full, [1.0])
+        st.verify()
+        st.lm_head()
+        r = rows + (k - 1)
+        p = torch.exp(st.logits[r] * (1.0 / st.temperature) - st.lse[r][:, None])
+        ck = c[:, k - 1]
+        qk = p * ck[:, None]
+        qk[torch.arange(B, device=st.device), w[:, k - 1]] += 1.0 - ck
+        st.q[:, k - 1].copy_(qk)
+        g = st.argmax.cpu().numpy().reshape(B, D + 1)
+        hit = match_u[:, k - 1] < conf[:, k - 1]
+        z[hit, k] = g[hit, k - 1]
+    st.set_draft(z)
+    st.seed = keep_seed
+    torch.cuda.synchronize()
     return z

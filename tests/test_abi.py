@@ -62,8 +62,9 @@ def test_workspace_sizes():
     assert L.workspace_bytes(3, None, 64, 15) == 0
     ws1 = L.workspace_bytes(1, cfg, 64, 15)
     assert 0 < ws1 < (1 << 31) and ws1 % 256 == 0
-    # normalised rows plus up to one key per row and 64 columns of the vocabulary
-    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 1024 * 2 * ((cfg.vocab + 127) // 128) * 8
+    # normalised rows plus, per row and 64 columns of the vocabulary, one key and one
+    # (max, sum) pair of the log-partition function
+    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 2 * 1024 * 2 * ((cfg.vocab + 127) // 128) * 8
     # RS acceptance: two int32 per request plus one key per request and 2048-column chunk
     nch = (cfg.vocab + 2047) // 2048
     assert L.workspace_bytes(4, cfg, 64, 15) >= 64 * 8 + 64 * nch * 8
@@ -135,7 +136,6 @@ def test_other_entry_points_reject_invalid_args():
     assert smp(fake, fake, float("inf"), 1 << 30) == L.EINVAL
     assert smp(fake, fake, float("nan"), 1 << 30) == L.EINVAL
     assert smp(fake, fake, 1.0, 0) == L.EWORKSPACE
-    assert smp(fake, fake, 1.0, 1 << 30, lg=None, lse=fake) == L.EINVAL      # lse needs the logits
     cfg = L.LayerCfg(256, 4, 2, 64, 688, 0, 0, 0, 1024, 160, 1e-5, 5e5)
     w = L.LayerW(*([0x1000] * 7 + [None] * 3))
     kv = L.KV(0x1000, 0x1000, 0x1000, 0x1000)
