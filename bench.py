@@ -168,6 +168,12 @@ def main():
                     help="rejection-sampling verification (dcut_select_rs with the causal scan, "
                          "dcut_lm_head_sample with logits, dcut_accept_rs) against a synthetic stochastic "
                          "drafter; temperature 1 unless --temperature is given")
+    ap.add_argument("--graph", action="store_true",
+                    help="also capture the adaptive step into a HIP graph and time its replays "
+                         "(reported as graph_ms_per_step beside the eager figures)")
+    ap.add_argument("--cost-table", action="store_true",
+                    help="run the startup cost-table protocol over captured batch sizes 1, 8, 16, 32, 64 and "
+                         "the ratio buckets 25/50/75/100 %% (each entry a graph-captured step, median of 10)")
     ap.add_argument("--state", default=None,
                     help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
                          "run of the same workload; written when missing, reused when present (a "
@@ -292,6 +298,50 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     L.profile_arm("NONE")
+    graph = None
+    if args.graph:
+        g = vs.capture(adaptive)
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        ga, gb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ga.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        gb.record(stream)
+        torch.cuda.synchronize()
+        gms = ga.elapsed_time(gb) / args.steps
+        graph = dict(ms_per_step=round(gms, 4), tokens_per_s=round(int(vs.total.item()) / (gms * 1e-3), 1))
+        log(f"graph replay: {gms:.4f} ms per step")
+        del g
+    table = None
+    if args.cost_table:
+        from paper_2607_14647_amd import costtable as ct
+        import dataclasses as dc
+        steps, keep = {}, []
+        for Bc in (1, 8, 16, 32, 64):
+            c2 = dc.replace(cfg, B=Bc, budgets=tuple(Bc * m for m in range(1, cfg.D + 2)))
+            st2 = wl.make_step_inputs(c2, args.seed)
+            kv2 = wl.make_kv(c2, args.seed, st2["ctx_len"])
+            v2 = runner.VerifyStep(c2, None, st2, kv2, share_weights=vs)
+            runner.force_drafts_on_device(v2, st2["draft"], st2["conf"], st2["match_u"])
+            graphs = {}
+
+            def run(budgets, v2=v2, graphs=graphs):
+                K = budgets[0]
+                if K not in graphs:
+                    graphs[K] = v2.capture(lambda: v2.step([K], [1.0]))
+                graphs[K].replay()
+            steps[Bc] = run
+            keep.append((v2, graphs))
+        log("cost table: captured batch sizes 1, 8, 16, 32, 64 x ratios 25/50/75/100 %")
+        t = ct.profile(steps, cfg.D, ct.PAPER_RATIOS, time_ms=ct.event_timer(stream), reps=10, warmup=2)
+        table = dict(D=t.D, ratios=t.ratios, batch=t.batch, ms=[[round(x, 4) for x in r] for r in t.ms],
+                     budgets={B: t.budgets(B) for B in t.batch},
+                     nearest={B: t.row(B)[0] for B in (4, 12, 24, 40, 48, 100)})
+        log("cost table (ms): " + "; ".join(f"B={B}: " + ", ".join(f"{x:.3f}" for x in r)
+                                             for B, r in zip(t.batch, t.ms)))
+        del keep, steps
     if args.copy_bytes > 0:
         src = torch.ones(args.copy_bytes, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -347,6 +397,10 @@ def main():
         fixed_ratio=fixed,
         source_hash=source_hash(),
     )
+    if graph is not None:
+        out["graph"] = graph
+    if table is not None:
+        out["cost_table"] = table
     if not args.no_cpu_baseline and args.temperature == 0:
         out["cpu_baseline"] = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
     else:

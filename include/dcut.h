@@ -129,21 +129,31 @@ int dcut_select(int B, int D, const float *conf, const int32_t *draft, const int
  *                    C(K) = C_r + ((C_{r+1} - C_r) * (K - K_r)) / (K_{r+1} - K_r),
  *                    float64 in that order.  choice = {K*, the last r with
  *                    K_r <= K*, or -1}.
- *     DCUT_RS_FIXED  a budget fixed before the block was drafted (for example
- *                    from earlier steps' statistics): R must be 1 and K* = K_0,
- *                    the global top-K_0 of the shifted scores; choice = {K_0, 0}.
+ *     DCUT_RS_FIXED  a budget fixed before the block was drafted: R must be 1
+ *                    and K* = K_0, the global top-K_0 of the shifted scores;
+ *                    choice = {K_0, 0}.
+ *     DCUT_RS_HISTORY  a budget carried over from the previous step (history-
+ *                    based K): K* = k_state[0] clamped to [B, B(D+1)], the
+ *                    global top-K* of the shifted scores; then k_state[0]
+ *                    becomes the budget the cost model picks for this block
+ *                    (the first strict maximum of benefit_r * 2^-40 / costs[r],
+ *                    as in dcut_select, on the shifted scores), the next
+ *                    step's budget.  choice = {K*, the last r with K_r <= K*,
+ *                    or -1}.
  * The paper takes c_{i,k} = q_{i,k}(z_{i,k}), the drafter's probability of its
  * own proposal; causality needs only that c_{i,k} depend on no proposal after
  * z_{i,k}.
  *
- *   mode      DCUT_RS_SCAN or DCUT_RS_FIXED
+ *   mode      DCUT_RS_SCAN, DCUT_RS_FIXED or DCUT_RS_HISTORY
+ *   k_state   dev [1] int32, read and written by DCUT_RS_HISTORY (the caller
+ *             sets the first step's budget), ignored (may be NULL) otherwise
  *   every other argument as for dcut_select (benefit[r] sums shifted scores)
- * Returns DCUT_OK, DCUT_EINVAL (also for an unknown mode, or R != 1 with
- * DCUT_RS_FIXED), DCUT_EHIP.
+ * Returns DCUT_OK, DCUT_EINVAL (also for an unknown mode, R != 1 with
+ * DCUT_RS_FIXED, or a NULL k_state with DCUT_RS_HISTORY), DCUT_EHIP.
  */
-enum { DCUT_RS_SCAN = 0, DCUT_RS_FIXED = 1 };
+enum { DCUT_RS_SCAN = 0, DCUT_RS_FIXED = 1, DCUT_RS_HISTORY = 2 };
 int dcut_select_rs(int B, int D, const float *conf, const int32_t *draft, const int32_t *ctx_len,
-                   int mode, int R, const int32_t *budgets, const double *costs,
+                   int mode, int R, const int32_t *budgets, const double *costs, int32_t *k_state,
                    int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
                    int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
                    hipStream_t stream);

@@ -33,6 +33,10 @@ Readings fixed here where the paper leaves the arithmetic open:
     consecutive budgets (K_r, C_r) and is constant outside [K_0, K_{R-1}];
     where several budgets coincide, the last one's cost holds at that K;
   * the fixed-budget variant takes exactly one budget;
+  * history-based K: the budget of this step is the one the cost model picks
+    (Eq. dcut-objective over the candidate budgets, first strict maximum)
+    on the previous step's shifted scores, carried in one integer of state
+    (clamped to [B, B(D+1)]); it is fixed before the current block is seen;
   * the target distribution of a kept row is softmax(logits / T);
     acceptance compares u * q(z) < p(z) in float64, with u one Philox4x32-10
     uniform per row (counter (0, pos, req, 1), word 0, u = (w + 0.5) / 2^32);
@@ -55,7 +59,8 @@ from .sampling import gumbel, philox4x32_10
 from .select import FIX_SHIFT, check_args, fixed_point
 
 SCAN = 0        # causal early-stopping scan over the interpolated cost curve
-FIXED = 1       # budget fixed beforehand (history-based K), global top-K
+FIXED = 1       # budget fixed beforehand, global top-K
+HISTORY = 2     # budget carried over from the previous block, global top-K
 
 
 def shifted_scores(conf: np.ndarray) -> np.ndarray:
@@ -162,18 +167,19 @@ def _pack(draft, ctx_len, keep_len):
 
 
 def select_rs(conf: np.ndarray, draft: np.ndarray, ctx_len: np.ndarray, mode: int,
-              budgets: Sequence[int], costs: Sequence[float]) -> Dict[str, np.ndarray]:
+              budgets: Sequence[int], costs: Sequence[float], k_state: int = 0) -> Dict[str, np.ndarray]:
     """RS-safe selection and packing; the same outputs as the unshifted selection.
 
     choice = (K*, r) with r the last budget index whose K_r <= K* (-1 if none);
     benefit[r] = exact fixed-point sum of the shifted scores over the top-K_r
-    positions of the global ranking."""
+    positions of the global ranking.  With HISTORY, K* = k_state clamped to
+    [B, B(D+1)], and k_next is the budget for the next step."""
     conf = np.asarray(conf, dtype=np.float32)
     draft = np.asarray(draft)
     B, D = conf.shape
     check_args(B, D, budgets, costs)
-    if mode not in (SCAN, FIXED):
-        raise DcutArgError("mode must be SCAN or FIXED")
+    if mode not in (SCAN, FIXED, HISTORY):
+        raise DcutArgError("mode must be SCAN, FIXED or HISTORY")
     if mode == FIXED and len(budgets) != 1:
         raise DcutArgError("a fixed budget takes exactly one candidate")
     s = shifted_scores(conf)
@@ -183,16 +189,25 @@ def select_rs(conf: np.ndarray, draft: np.ndarray, ctx_len: np.ndarray, mode: in
     P = np.zeros(B * (D + 1) + 1, dtype=np.uint64)
     P[1:] = np.cumsum(u[order], dtype=np.uint64)
     benefit = np.array([P[K] for K in budgets], dtype=np.uint64)
+    k_next = None
+    if mode == HISTORY:
+        # this block's retrospective choice, the budget of the next step
+        best_r, best_obj = 0, -1.0
+        for r, (K, C) in enumerate(zip(budgets, costs)):
+            obj = _objective(int(P[K]), float(C))
+            if obj > best_obj:
+                best_r, best_obj = r, obj
+        k_next = int(budgets[best_r])
     if mode == SCAN:
         sc = causal_scan(s, cost_curve(B, D, budgets, costs))
         Kstar, kept = int(sc["K"]), sc["admitted"]
         objective = sc["objective"]
     else:
-        Kstar = int(budgets[0])
+        Kstar = int(budgets[0]) if mode == FIXED else min(max(int(k_state), B), B * (D + 1))
         kept = np.zeros(B * (D + 1), dtype=bool)
         kept[order[:Kstar]] = True
         kept = kept.reshape(B, D + 1)
-        objective = _objective(int(P[Kstar]), float(costs[0]))
+        objective = _objective(int(P[Kstar]), float(costs[0])) if mode == FIXED else None
     keep_len = kept.sum(axis=1).astype(np.int32)
     for i in range(B):            # kept positions form a prefix (s~ is non-increasing in depth)
         assert kept[i, : keep_len[i]].all() and not kept[i, keep_len[i]:].any()
@@ -203,7 +218,7 @@ def select_rs(conf: np.ndarray, draft: np.ndarray, ctx_len: np.ndarray, mode: in
     cu, ptok, ppos, preq = _pack(draft, ctx_len, keep_len)
     return dict(scores=s, keep_len=keep_len, cu=cu, packed_tok=ptok, packed_pos=ppos,
                 packed_req=preq, choice=np.array([Kstar, r_of], dtype=np.int32),
-                benefit=benefit, objective=objective, kept=kept)
+                benefit=benefit, objective=objective, kept=kept, k_next=k_next)
 
 
 def accept_uniform(req, pos, seed: int) -> np.ndarray:

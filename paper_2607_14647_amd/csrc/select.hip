@@ -18,7 +18,7 @@
 
 namespace dcut {
 
-enum SelectMode { SEL_BUCKETS = 0, SEL_SCAN = 1, SEL_FIXED = 2 };
+enum SelectMode { SEL_BUCKETS = 0, SEL_SCAN = 1, SEL_FIXED = 2, SEL_HISTORY = 3 };
 
 struct SelectParams {
   int B, D, R;
@@ -65,7 +65,7 @@ __device__ __forceinline__ double objective(unsigned long long P, double cost) {
 __global__ void __launch_bounds__(1024)
 k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ keep_len,
          int32_t *__restrict__ choice, unsigned long long *__restrict__ benefit,
-         int32_t *__restrict__ dev_err) {
+         int32_t *__restrict__ dev_err, int32_t *__restrict__ k_state) {
   extern __shared__ unsigned long long smem[];
   __shared__ unsigned long long s_wave[17];
   __shared__ unsigned long long s_ben[DCUT_MAX_CANDIDATES];
@@ -185,24 +185,33 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   }
   __syncthreads();
 
-  // 4b. budget choice: the scan's stop, the fixed budget, or the first strict
-  // maximum of benefit * 2^-40 / cost over the candidates
+  // 4b. budget choice: the first strict maximum of benefit * 2^-40 / cost over
+  // the candidates, the fixed budget, the scan's stop, or the budget carried
+  // over from the previous block (which then carries this block's choice on)
   if (tid == 0) {
     int best = 0, Kstar;
-    if (p.mode == SEL_BUCKETS) {
-      double best_obj = -1.0;
-      for (int r = 0; r < p.R; ++r) {
-        double obj = objective(s_ben[r], p.costs[r]);
-        if (obj > best_obj) {
-          best_obj = obj;
-          best = r;
-        }
+    int bucket = 0;                   // first strict maximum of the objective over the candidates
+    double best_obj = -1.0;
+    for (int r = 0; r < p.R; ++r) {
+      double obj = objective(s_ben[r], p.costs[r]);
+      if (obj > best_obj) {
+        best_obj = obj;
+        bucket = r;
       }
+    }
+    if (p.mode == SEL_BUCKETS) {
+      best = bucket;
       Kstar = p.budgets[best];
     } else if (p.mode == SEL_FIXED) {
       Kstar = p.budgets[0];
     } else {
-      Kstar = s_stop;
+      if (p.mode == SEL_SCAN) {
+        Kstar = s_stop;
+      } else {
+        const int k = k_state[0];
+        Kstar = k < B ? B : (k > N ? N : k);
+        k_state[0] = p.budgets[bucket];
+      }
       best = -1;                      // the last candidate budget not above K*
       for (int r = 0; r < p.R; ++r)
         if (p.budgets[r] <= Kstar) best = r;
@@ -278,13 +287,14 @@ k_pack(int B, int D, const int32_t *__restrict__ keep_len, const int32_t *__rest
 using namespace dcut;
 
 static int select_run(int B, int D, const float *conf, const int32_t *draft, const int32_t *ctx_len,
-                      int shift, int mode, int R, const int32_t *budgets, const double *costs,
+                      int shift, int mode, int R, const int32_t *budgets, const double *costs, int32_t *k_state,
                       int32_t *keep_len, int32_t *cu, int32_t *packed_tok, int32_t *packed_pos,
                       int32_t *packed_req, int32_t *choice, uint64_t *benefit, int32_t *dev_err,
                       hipStream_t stream) {
   if (!batch_ok(B, D)) return DCUT_EINVAL;
   if (R < 1 || R > DCUT_MAX_CANDIDATES || !budgets || !costs) return DCUT_EINVAL;
   if (mode == SEL_FIXED && R != 1) return DCUT_EINVAL;
+  if (mode == SEL_HISTORY && !k_state) return DCUT_EINVAL;
   if (!conf && D > 0) return DCUT_EINVAL;
   if (!draft || !ctx_len || !keep_len || !cu || !packed_tok || !packed_pos || !packed_req || !choice)
     return DCUT_EINVAL;
@@ -307,7 +317,7 @@ static int select_run(int B, int D, const float *conf, const int32_t *draft, con
   while (NP < N) NP <<= 1;
   size_t shmem = (size_t)(NP + 1024) * sizeof(unsigned long long) + (size_t)B * D * sizeof(float);
   DCUT_TRY(launch(DCUT_KERNEL_SELECT, k_select, dim3(1), dim3(1024), shmem, stream, p, conf,
-                  keep_len, choice, (unsigned long long *)benefit, dev_err));
+                  keep_len, choice, (unsigned long long *)benefit, dev_err, k_state));
   DCUT_TRY(launch(DCUT_KERNEL_PACK, k_pack, dim3(1), dim3(1024), 0, stream, B, D,
                   (const int32_t *)keep_len, draft, ctx_len, cu, packed_tok, packed_pos, packed_req));
   return DCUT_OK;
@@ -319,20 +329,21 @@ extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft
                            int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
                            int32_t *choice, uint64_t *benefit, int32_t *dev_err,
                            hipStream_t stream) {
-  return select_run(B, D, conf, draft, ctx_len, 0, SEL_BUCKETS, R, budgets, costs, keep_len, cu,
+  return select_run(B, D, conf, draft, ctx_len, 0, SEL_BUCKETS, R, budgets, costs, nullptr, keep_len, cu,
                     packed_tok, packed_pos, packed_req, choice, benefit, dev_err, stream);
 }
 
 extern "C" int dcut_select_rs(int B, int D, const float *conf, const int32_t *draft,
                               const int32_t *ctx_len, int mode, int R, const int32_t *budgets,
-                              const double *costs, int32_t *keep_len, int32_t *cu,
+                              const double *costs, int32_t *k_state, int32_t *keep_len, int32_t *cu,
                               int32_t *packed_tok, int32_t *packed_pos, int32_t *packed_req,
                               int32_t *choice, uint64_t *benefit, int32_t *dev_err,
                               hipStream_t stream) {
   int m;
   if (mode == DCUT_RS_SCAN) m = SEL_SCAN;
   else if (mode == DCUT_RS_FIXED) m = SEL_FIXED;
+  else if (mode == DCUT_RS_HISTORY) m = SEL_HISTORY;
   else return DCUT_EINVAL;
-  return select_run(B, D, conf, draft, ctx_len, 1, m, R, budgets, costs, keep_len, cu, packed_tok,
+  return select_run(B, D, conf, draft, ctx_len, 1, m, R, budgets, costs, k_state, keep_len, cu, packed_tok,
                     packed_pos, packed_req, choice, benefit, dev_err, stream);
 }

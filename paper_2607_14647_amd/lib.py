@@ -21,7 +21,7 @@ DERR_CONF, DERR_TOKEN, DERR_CAPACITY = 1, 2, 4
 KERNELS = dict(NONE=0, SELECT=1, PACK=2, NORM=3, GEMM_QKV=4, ATTN=5, ATTN_COMBINE=6, GEMM_O=7,
                GEMM_GATE_UP=8, GEMM_DOWN=9, MOE=10, LM_HEAD=11, ARGMAX_FINAL=12, ACCEPT=13,
                RS_DECIDE=14, RS_RESIDUAL=15, RS_FINISH=16)
-RS_SCAN, RS_FIXED = 0, 1
+RS_SCAN, RS_FIXED, RS_HISTORY = 0, 1, 2
 
 EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",
            "dcut_lm_head_sample", "dcut_select_rs", "dcut_accept_rs", "dcut_workspace_bytes", "dcut_strerror",
@@ -65,7 +65,7 @@ def _load() -> C.CDLL:
     lib.dcut_lm_head_sample.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, C.c_float, vp, C.c_float,
                                         C.c_uint64, vp, vp, vp, vp, vp, sz, vp]
     lib.dcut_accept.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
-    lib.dcut_select_rs.argtypes = [i32, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.dcut_select_rs.argtypes = [i32, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.dcut_accept_rs.argtypes = [i32, i32, i32, C.c_float, C.c_uint64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    vp, vp, vp, vp, sz, vp, vp]
     lib.dcut_workspace_bytes.argtypes = [i32, C.POINTER(LayerCfg), i32, i32]
@@ -158,12 +158,13 @@ def select(B: int, D: int, conf: torch.Tensor, draft: torch.Tensor, ctx_len: tor
 
 def select_rs(B: int, D: int, conf: torch.Tensor, draft: torch.Tensor, ctx_len: torch.Tensor, mode: int,
               budgets: Sequence[int], costs: Sequence[float], out: Dict[str, torch.Tensor],
-              dev_err: Optional[torch.Tensor] = None, stream=None) -> None:
+              dev_err: Optional[torch.Tensor] = None, k_state: Optional[torch.Tensor] = None,
+              stream=None) -> None:
     R = len(budgets)
     b = (C.c_int32 * max(R, 1))(*[int(x) for x in budgets])
     c = (C.c_double * max(R, 1))(*[float(x) for x in costs])
     st = _lib.dcut_select_rs(B, D, _p(conf), _p(draft), _p(ctx_len), int(mode), R, C.cast(b, C.c_void_p),
-                             C.cast(c, C.c_void_p), _p(out["keep_len"]), _p(out["cu"]),
+                             C.cast(c, C.c_void_p), _p(k_state), _p(out["keep_len"]), _p(out["cu"]),
                              _p(out["packed_tok"]), _p(out["packed_pos"]), _p(out["packed_req"]),
                              _p(out["choice"]), _p(out.get("benefit")), _p(dev_err), _stream(stream))
     _check(st, "dcut_select_rs")

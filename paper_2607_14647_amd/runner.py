@@ -23,14 +23,19 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
 
 class VerifyStep:
     def __init__(self, cfg: wl.Config, weights: Dict[str, np.ndarray], step: Dict[str, np.ndarray],
-                 kv: Dict[str, np.ndarray], device: str = "cuda", R_max: int = 64):
+                 kv: Dict[str, np.ndarray], device: str = "cuda", R_max: int = 64,
+                 share_weights: Optional["VerifyStep"] = None):
         self.cfg = cfg
         self.B, self.D = cfg.B, cfg.D
         self.rows = cfg.B * (cfg.D + 1)
         ly = cfg.layer
         self.ly = ly
         self.device = device
-        self.w = {k: _dev(v, device) for k, v in weights.items()}
+        if share_weights is not None:          # another batch size of the same model
+            assert share_weights.ly == ly
+            self.w = share_weights.w
+        else:
+            self.w = {k: _dev(v, device) for k, v in weights.items()}
         self.lw = L.layer_weights(self.w)
         self.conf = _dev(step["conf"], device)
         self.draft = _dev(step["draft"], device)
@@ -52,6 +57,8 @@ class VerifyStep:
         self.temperature = 0.0      # > 0: temperature sampling instead of the greedy argmax
         self.seed = 0
         self.q = None               # proposal distributions [B][D][V]: rejection-sampling verification
+        self.rs_mode = L.RS_SCAN    # budget choice of step_rs with several candidates
+        self.k_state = torch.zeros(1, **i32)   # history-based budget carried between steps
 
     def enable_rs(self, q) -> None:
         """Switch to rejection-sampling verification with proposal distributions q [B][D][V]
@@ -78,7 +85,7 @@ class VerifyStep:
 
     def select_rs(self, mode: int, budgets: Sequence[int], costs: Sequence[float]) -> None:
         L.select_rs(self.B, self.D, self.conf, self.draft, self.ctx_len, mode, budgets, costs, self.sel,
-                    self.dev_err)
+                    self.dev_err, k_state=self.k_state)
 
     def verify(self, x_in: Optional[torch.Tensor] = None) -> None:
         L.verify_layer(self.lcfg, self.lw, self.B, self.D, self.sel, self.ctx_len, self.kvd, self.x,
@@ -116,12 +123,29 @@ class VerifyStep:
         self.accept()
 
     def step_rs(self, budgets: Sequence[int], costs: Sequence[float]) -> None:
-        """One rejection-sampling step: the causal scan over the candidates, or
-        the fixed budget when only one is given."""
-        self.select_rs(L.RS_FIXED if len(budgets) == 1 else L.RS_SCAN, budgets, costs)
+        """One rejection-sampling step: `rs_mode` over the candidates (the causal
+        scan or the history-based budget), or the fixed budget when only one is given."""
+        self.select_rs(L.RS_FIXED if len(budgets) == 1 else self.rs_mode, budgets, costs)
         self.verify()
         self.lm_head()
         self.accept_rs()
+
+    def capture(self, fn) -> "torch.cuda.CUDAGraph":
+        """Capture the library calls `fn` makes into one HIP graph (stream capture
+        through torch.cuda.graph on a default-priority side stream); replay it
+        with .replay().  The calls take every size from the host and K* from the
+        device, so one graph per batch size serves every budget the step picks."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):          # one eager pass first (kernel attributes, caches)
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        return g
 
     def host(self, name: str) -> np.ndarray:
         src = self.sel[name] if name in self.sel else getattr(self, name)

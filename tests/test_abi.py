@@ -95,22 +95,23 @@ def test_select_rejects_invalid_args(B, D, R, budgets, costs):
     assert _sel_call(B, D, R, budgets, costs) == L.EINVAL
 
 
-def _sel_rs_call(mode, R, budgets, costs):
+def _sel_rs_call(mode, R, budgets, costs, k_state=None):
     lib = L.lib()
     b = (C.c_int32 * max(R, 1))(*budgets)
     c = (C.c_double * max(R, 1))(*costs)
     fake = C.c_void_p(0x1000)
     return lib.dcut_select_rs(4, 15, fake, fake, fake, mode, R, C.cast(b, C.c_void_p), C.cast(c, C.c_void_p),
-                              fake, fake, fake, fake, fake, fake, None, None, None)
+                              k_state, fake, fake, fake, fake, fake, fake, None, None, None)
 
 
 def test_select_rs_rejects_invalid_args():
-    assert _sel_rs_call(2, 1, [8], [1.0]) == L.EINVAL                      # unknown mode
     assert _sel_rs_call(-1, 1, [8], [1.0]) == L.EINVAL
     assert _sel_rs_call(L.RS_FIXED, 2, [8, 16], [1.0, 2.0]) == L.EINVAL    # a fixed budget is one budget
     assert _sel_rs_call(L.RS_SCAN, 1, [3], [1.0]) == L.EINVAL              # below B
     assert _sel_rs_call(L.RS_SCAN, 2, [16, 8], [1.0, 2.0]) == L.EINVAL     # decreasing
     assert _sel_rs_call(L.RS_SCAN, 1, [8], [0.0]) == L.EINVAL
+    assert _sel_rs_call(L.RS_HISTORY, 2, [8, 16], [1.0, 2.0]) == L.EINVAL   # history needs its state word
+    assert _sel_rs_call(3, 1, [8], [1.0]) == L.EINVAL
 
 
 def test_select_rejects_null_outputs():

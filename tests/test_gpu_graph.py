@@ -1,0 +1,95 @@
+"""Whole verify steps captured into HIP graphs replay the eager results bit for bit.
+
+One graph per batch size: every size the calls take comes from the host and
+K* stays on the device, so a captured adaptive step picks its budget anew on
+each replay.  Each replay follows eager work that overwrites the outputs (a
+different budget), and every replay is compared with the eager step.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_14647_amd import lib as L
+from paper_2607_14647_amd import runner
+from paper_2607_14647_amd import workload as wl
+from tests.gpu_common import need_gpu, note, tiny_variants, workload
+
+pytestmark = pytest.mark.gpu
+VARIANTS = tiny_variants()
+
+
+def _snapshot(vs):
+    K = int(vs.sel["cu"][-1].item())
+    out = {k: vs.host(k) for k in ("choice", "keep_len", "cu", "accept_len", "next_tok", "total")}
+    out["argmax"] = vs.host("argmax")[:K]
+    out["x"] = vs.x[:K].cpu().numpy()
+    if vs.q is not None:
+        out["lse"] = vs.lse[:K].cpu().numpy()
+        out["k_state"] = vs.k_state.cpu().numpy()
+    return out
+
+
+def _same(a, b):
+    assert a.keys() == b.keys()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def _candidates(cfg):
+    N = cfg.B * (cfg.D + 1)
+    budgets = sorted({cfg.B, cfg.budgets[0], (cfg.B + N) // 2, N})
+    costs = [1.0 + 0.002 * K + (0.5 if K > cfg.budgets[0] else 0.0) for K in budgets]
+    return budgets, costs
+
+
+@pytest.mark.parametrize("name", ["cfg1", "split", "moe", "long"])
+def test_graph_greedy_step(name):
+    need_gpu()
+    cfg = VARIANTS[name]
+    st, w, kv = workload(cfg, 0)
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    budgets, costs = _candidates(cfg)
+    step = lambda: vs.step(budgets, costs)
+    step()
+    torch.cuda.synchronize()
+    ref = _snapshot(vs)
+    note(f"graph greedy {name}: K*={ref['choice'][0]}")
+    g = vs.capture(step)
+    for rep in range(3):
+        vs.step([cfg.B * (cfg.D + 1)], [1.0])          # eager work that overwrites every output
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _same(_snapshot(vs), ref)
+
+
+@pytest.mark.parametrize("mode", [L.RS_SCAN, L.RS_HISTORY])
+def test_graph_rs_step(mode):
+    need_gpu()
+    cfg = VARIANTS["cfg1"]
+    st, w, kv = workload(cfg, 0)
+    prop = wl.make_proposals(cfg, 0, st["draft"][:, 0])
+    st = dict(st, conf=prop["conf"], draft=prop["draft"])
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    vs.enable_rs(prop["q"])
+    vs.temperature, vs.seed, vs.rs_mode = 1.0, 99, mode
+    budgets, costs = _candidates(cfg)
+    step = lambda: vs.step_rs(budgets, costs)
+    # eager sequence (the history mode carries its budget from step to step)
+    vs.k_state.fill_(budgets[-1])
+    eager = []
+    for _ in range(3):
+        step()
+        torch.cuda.synchronize()
+        eager.append(_snapshot(vs))
+    note(f"graph rs mode {mode}: K* per step {[int(e['choice'][0]) for e in eager]}")
+    vs.k_state.fill_(budgets[-1])
+    g = vs.capture(step)                 # capture runs the step once more: restart the state
+    for rep in range(3):
+        if rep == 0:
+            vs.k_state.fill_(budgets[-1])
+        vs.step([cfg.B], [1.0])           # eager greedy-budget work in between
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _same(_snapshot(vs), eager[rep])

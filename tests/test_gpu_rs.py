@@ -36,13 +36,13 @@ SEED = 0x51D_0_5EED
 
 # ---------------------------------------------------------------- selection
 
-def gpu_select_rs(conf, draft, ctx, mode, budgets, costs):
+def gpu_select_rs(conf, draft, ctx, mode, budgets, costs, k_state=None):
     B, D1 = draft.shape
     D = D1 - 1
     out = L.select_outputs(B, D, len(budgets))
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     c = to_dev(conf.astype(np.float32)) if D > 0 else torch.zeros(1, device="cuda")
-    L.select_rs(B, D, c, to_dev(draft), to_dev(ctx), mode, budgets, costs, out, err)
+    L.select_rs(B, D, c, to_dev(draft), to_dev(ctx), mode, budgets, costs, out, err, k_state=k_state)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}, int(err.item())
 
@@ -86,6 +86,30 @@ def test_select_rs_configs(cid, seed):
     check_select(st["conf"], st["draft"], st["ctx_len"], L.RS_SCAN, budgets, _costs(rng, budgets, False))
     K = int(rng.integers(cfg.B, cfg.B * (cfg.D + 1) + 1))
     check_select(st["conf"], st["draft"], st["ctx_len"], L.RS_FIXED, [K], [1.0])
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_select_rs_history_chain(cid):
+    """History-based K over four consecutive blocks: each step's budget is the
+    previous block's choice, carried in the device state word."""
+    need_gpu()
+    cfg = wl.CONFIGS[cid]
+    budgets = list(cfg.budgets) if len(cfg.budgets) > 1 else [cfg.B, cfg.budgets[0], cfg.B * (cfg.D + 1)]
+    rng = np.random.default_rng(77 + cid)
+    costs = _costs(rng, budgets)
+    k_state = torch.full((1,), budgets[-1], dtype=torch.int32, device="cuda")
+    k_ref = budgets[-1]
+    for t in range(4):
+        st = wl.make_step_inputs(cfg, 100 + t)
+        got, err = gpu_select_rs(st["conf"], st["draft"], st["ctx_len"], L.RS_HISTORY, budgets, costs, k_state)
+        ref = ors.select_rs(st["conf"], st["draft"], st["ctx_len"], ors.HISTORY, budgets, costs, k_state=k_ref)
+        note(f"history cfg{cid} step {t}: K*={int(ref['choice'][0])} next={ref['k_next']}")
+        assert err == 0
+        assert got["choice"].tolist() == ref["choice"].tolist()
+        assert np.array_equal(got["keep_len"], ref["keep_len"])
+        assert np.array_equal(got["benefit"][: len(budgets)].view(np.uint64), ref["benefit"])
+        assert int(k_state.item()) == ref["k_next"]
+        k_ref = ref["k_next"]
 
 
 def test_select_rs_hand_example():

@@ -241,6 +241,39 @@ def test_fixed_budget_is_global_top_k_of_shifted_scores():
                 assert (o["packed_tok"][t], o["packed_pos"][t], o["packed_req"][t]) == (z[i, k], L[i] + k, i)
 
 
+def test_history_budget_is_carried_and_causal():
+    """HISTORY: K* is the state passed in (clamped), retention is then causal,
+    and the state passed on is the retrospective bucket choice of this block
+    (brute force over the candidate budgets)."""
+    rng = np.random.default_rng(13)
+    for _ in range(60):
+        B, D, R = int(rng.integers(1, 6)), int(rng.integers(0, 6)), int(rng.integers(1, 5))
+        conf, budgets, costs = _random_instance(rng, B, D, R)
+        N = B * (D + 1)
+        z = np.zeros((B, D + 1), np.int32)
+        L = np.zeros(B, np.int32)
+        k_in = int(rng.integers(-3, N + 5))
+        o = rs.select_rs(conf, z, L, rs.HISTORY, budgets, costs, k_state=k_in)
+        assert int(o["choice"][0]) == min(max(k_in, B), N)
+        fx = rs.select_rs(conf, z, L, rs.FIXED, [min(max(k_in, B), N)], [1.0])
+        assert np.array_equal(o["kept"], fx["kept"])
+        # brute force: objective of every candidate from its own top-K sum
+        s = rs.shifted_scores(conf)
+        vals = sorted(((float(s[i, k]), -k, -i) for i in range(B) for k in range(D + 1)), reverse=True)
+        u = [int(np.trunc(np.float64(v[0]) * 2.0 ** 40)) for v in vals]
+        objs = [(float(sum(u[:K])) * 2.0 ** -40) / c for K, c in zip(budgets, costs)]
+        best = max(range(R), key=lambda r: (objs[r], -r))
+        assert o["k_next"] == budgets[best]
+    rng = np.random.default_rng(14)
+    assert _violations(lambda c, b, co: _retention_hist(c, b, co), rng, 80) == 0
+
+
+def _retention_hist(conf, budgets, costs):
+    B, D = conf.shape
+    return rs.select_rs(conf, np.zeros((B, D + 1), np.int32), np.zeros(B, np.int32), rs.HISTORY,
+                        budgets, costs, k_state=budgets[len(budgets) // 2])["kept"]
+
+
 def test_select_rs_argument_errors():
     conf = np.full((2, 3), 0.5, np.float32)
     z = np.zeros((2, 4), np.int32)
