@@ -168,6 +168,9 @@ def main():
                     help="rejection-sampling verification (dcut_select_rs with the causal scan, "
                          "dcut_lm_head_sample with logits, dcut_accept_rs) against a synthetic stochastic "
                          "drafter; temperature 1 unless --temperature is given")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="decoder layers in the verify pass (each with its own seeded weights and KV cache); "
+                         "32 is the full depth of the 8B-shaped target")
     ap.add_argument("--graph", action="store_true",
                     help="also capture the adaptive step into a HIP graph and time its replays "
                          "(reported as graph_ms_per_step beside the eager figures)")
@@ -203,6 +206,10 @@ def main():
     kv = wl.make_kv(cfg, args.seed, st["ctx_len"])
     log(f"generated in {time.time() - t0:.1f}s; uploading")
     vs = runner.VerifyStep(cfg, w, st, kv)
+    for l in range(1, args.layers):
+        vs.add_layer(wl.make_weights(cfg, args.seed, layer=l), wl.make_kv(cfg, args.seed, st["ctx_len"], layer=l))
+        if l % 8 == 0 or l == args.layers - 1:
+            log(f"layer {l} of {args.layers - 1} extra layers generated and uploaded")
     vs.temperature, vs.seed = float(args.temperature), int(args.sample_seed)
     torch.cuda.synchronize()
     budgets = list(cfg.budgets)
@@ -212,6 +219,7 @@ def main():
         assert state["workload"] == [cfg.cid, args.seed] and state["budgets"] == budgets, "state mismatch"
         assert state.get("temperature", 0.0) == args.temperature, "state mismatch (temperature)"
         assert state.get("rs", False) == args.rs, "state mismatch (rs)"
+        assert state.get("layers", 1) == args.layers, "state mismatch (layers)"
     if args.rs:
         vs.enable_rs(None)
         log("stochastic drafter: proposals and drafts from the target's own distributions (D passes)")
@@ -269,10 +277,12 @@ def main():
         L.profile_arm("NONE")
         torch.cuda.synchronize()
         breakdown[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
-    dominant = max(breakdown, key=lambda k: breakdown[k])
+    # the dominant kernel by time per step: layer kernels launch once per decoder layer
+    per_layer = {"GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "MOE"}
+    dominant = max(breakdown, key=lambda k: breakdown[k] * (args.layers if k in per_layer else 1))
     if args.state and state is None:
         json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,
-                       rs=args.rs,
+                       rs=args.rs, layers=args.layers,
                        accepted_per_budget=acc_per_k, kernel_us=breakdown,
                        draft=vs.host("draft").tolist()), open(args.state, "w"))
     log("kernel us: " + ", ".join(f"{k}={v}" for k, v in breakdown.items()) + f"; dominant {dominant}")
@@ -359,8 +369,9 @@ def main():
 
     # algorithmic bytes per step (weights, KV read, KV append, packed in/out)
     hd, nkv = ly.head_dim, ly.n_kv
-    wbytes = sum(int(w[k].size) * 2 for k in w if k != "embed") + Kstar * ly.hidden * 2
-    kvbytes = float(st["ctx_len"].astype(np.int64).sum()) * nkv * hd * 4 + Kstar * nkv * hd * 4
+    layer_w = sum(int(w[k].size) * 2 for k in w if k not in ("embed", "w_lm", "final_norm"))
+    wbytes = layer_w * args.layers + int(w["w_lm"].size) * 2 + Kstar * ly.hidden * 2
+    kvbytes = (float(st["ctx_len"].astype(np.int64).sum()) * nkv * hd * 4 + Kstar * nkv * hd * 4) * args.layers
     step_bytes = wbytes + kvbytes
     workload = f"cfg{cfg.cid}"
     rl = roofline(dominant, cfg, Kstar, st["ctx_len"], dom_us)
@@ -375,7 +386,9 @@ def main():
             fixed[rho] = dict(K=K, ms=round(cost_ms[j], 4), accepted=acc_per_k[j],
                               tokens_per_s=round(acc_per_k[j] / (cost_ms[j] * 1e-3), 1))
     out = dict(
-        metric="accepted tokens/s of pruned verify step (1 layer + LM head), batch 64; HBM GB/s",
+        metric="accepted tokens/s of pruned verify step (1 layer + LM head), batch 64; HBM GB/s"
+        if args.layers == 1 else
+        f"accepted tokens/s of pruned verify step ({args.layers} layers + LM head), batch 64; HBM GB/s",
         value=round(value, 1), unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
         ms_per_step=round(ms_per_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
         dtype="bf16", data="synthetic",
@@ -383,6 +396,7 @@ def main():
                              f"{ly.n_q}q/{ly.n_kv}kv hd{ly.head_dim}, I={ly.inter}, V={ly.vocab}, "
                              f"L~{cfg.ctx}, conf {cfg.conf_model}; seed {args.seed}",
                     global_batch=cfg.B, K_star=Kstar, r_star=rstar, accepted_per_step=accepted,
+                    layers=args.layers,
                     budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm",
                     target_decoding="greedy" if args.temperature == 0 else
                     (f"rejection sampling at temperature {args.temperature} (causal scan over shifted "
@@ -401,7 +415,7 @@ def main():
         out["graph"] = graph
     if table is not None:
         out["cost_table"] = table
-    if not args.no_cpu_baseline and args.temperature == 0:
+    if not args.no_cpu_baseline and args.temperature == 0 and args.layers == 1:
         out["cpu_baseline"] = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
     else:
         out["cpu_baseline"] = None

@@ -42,6 +42,7 @@ class VerifyStep:
         self.ctx_len = _dev(step["ctx_len"], device)
         self.kv = {k: _dev(v, device) for k, v in kv.items()}
         self.kvd = L.kv_desc(self.kv)
+        self.extra = []             # decoder layers after the first: (weights, descriptor, kv, kv descriptor)
         self.lcfg = L.layer_cfg(ly, int(kv["cap"].max()))
         self.sel = L.select_outputs(self.B, self.D, R_max, device)
         i32 = dict(dtype=torch.int32, device=device)
@@ -87,9 +88,19 @@ class VerifyStep:
         L.select_rs(self.B, self.D, self.conf, self.draft, self.ctx_len, mode, budgets, costs, self.sel,
                     self.dev_err, k_state=self.k_state)
 
+    def add_layer(self, weights: Dict[str, np.ndarray], kv: Dict[str, np.ndarray]) -> None:
+        """Append a decoder layer (its weights and KV cache) after the first: the
+        verify pass then runs every layer in order on the residual stream."""
+        w = {k: _dev(v, self.device) for k, v in weights.items()}
+        kvt = {k: _dev(v, self.device) for k, v in kv.items()}
+        self.extra.append((w, L.layer_weights(w), kvt, L.kv_desc(kvt)))
+
     def verify(self, x_in: Optional[torch.Tensor] = None) -> None:
         L.verify_layer(self.lcfg, self.lw, self.B, self.D, self.sel, self.ctx_len, self.kvd, self.x,
                        self.ws_layer, x_in=x_in, dev_err=self.dev_err)
+        for _, lw, _, kvd in self.extra:
+            L.verify_layer(self.lcfg, lw, self.B, self.D, self.sel, self.ctx_len, kvd, self.x,
+                           self.ws_layer, x_in=self.x, dev_err=self.dev_err)
 
     def lm_head(self, logits: Optional[torch.Tensor] = None) -> None:
         """Target token of every kept row into `argmax`: the greedy argmax, or a

@@ -120,15 +120,17 @@ def bf16_to_f32(u: np.ndarray) -> np.ndarray:
 
 
 def _normal_bf16(seed: int, cid: int, tag: str, n: int, std: float,
-                 workers: Optional[int] = None) -> np.ndarray:
-    """n samples of N(0, std^2), bf16-rounded, generated in fixed 4M-element streams."""
+                 workers: Optional[int] = None, layer: int = 0) -> np.ndarray:
+    """n samples of N(0, std^2), bf16-rounded, generated in fixed 4M-element streams
+    (decoder layer `layer` > 0 has streams of its own)."""
     out = np.empty(n, dtype=np.uint16)
     nchunks = (n + _CHUNK - 1) // _CHUNK
+    lx = () if layer == 0 else (1_000_000 + layer,)
 
     def work(c: int) -> None:
         lo = c * _CHUNK
         hi = min(n, lo + _CHUNK)
-        g = _gen(seed, cid, tag, c)
+        g = _gen(seed, cid, tag, c, *lx)
         v = g.standard_normal(hi - lo, dtype=np.float32)
         v *= np.float32(std)
         out[lo:hi] = bf16_round(v)
@@ -187,18 +189,18 @@ def kv_layout(cfg: Config, ctx_len: np.ndarray) -> Tuple[np.ndarray, np.ndarray,
     return cap.astype(np.int32), base, int(slab.sum())
 
 
-def make_kv_request(cfg: Config, seed: int, i: int, L: int, which: str) -> np.ndarray:
-    """Cached entries of request i: [n_kv][L][head_dim] raw bf16 bits."""
+def make_kv_request(cfg: Config, seed: int, i: int, L: int, which: str, layer: int = 0) -> np.ndarray:
+    """Cached entries of request i: [n_kv][L][head_dim] raw bf16 bits (of decoder layer `layer`)."""
     ly = cfg.layer
-    g = _gen(seed, cfg.cid, "kv_k" if which == "k" else "kv_v", i)
+    g = _gen(seed, cfg.cid, "kv_k" if which == "k" else "kv_v", i, *(() if layer == 0 else (1_000_000 + layer,)))
     v = g.standard_normal((ly.n_kv, L, ly.head_dim), dtype=np.float32)
     v *= np.float32(cfg.weight_std)
     return bf16_round(v).reshape(ly.n_kv, L, ly.head_dim)
 
 
 def make_kv(cfg: Config, seed: int, ctx_len: np.ndarray,
-            requests: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
-    """Full flat caches k, v (uint16 bf16 bits) with slots >= L_i zeroed."""
+            requests: Optional[np.ndarray] = None, layer: int = 0) -> Dict[str, np.ndarray]:
+    """Full flat caches k, v (uint16 bf16 bits) with slots >= L_i zeroed (of decoder layer `layer`)."""
     cap, base, total = kv_layout(cfg, ctx_len)
     ly = cfg.layer
     k = np.zeros(total, dtype=np.uint16)
@@ -210,8 +212,8 @@ def make_kv(cfg: Config, seed: int, ctx_len: np.ndarray,
         c = int(cap[i])
         sk = k[base[i]: base[i] + ly.n_kv * c * ly.head_dim].reshape(ly.n_kv, c, ly.head_dim)
         sv = v[base[i]: base[i] + ly.n_kv * c * ly.head_dim].reshape(ly.n_kv, c, ly.head_dim)
-        sk[:, :L, :] = make_kv_request(cfg, seed, i, L, "k")
-        sv[:, :L, :] = make_kv_request(cfg, seed, i, L, "v")
+        sk[:, :L, :] = make_kv_request(cfg, seed, i, L, "k", layer)
+        sv[:, :L, :] = make_kv_request(cfg, seed, i, L, "v", layer)
 
     workers = min(16, len(os.sched_getaffinity(0)))
     with _cf.ThreadPoolExecutor(workers) as ex:
@@ -219,12 +221,15 @@ def make_kv(cfg: Config, seed: int, ctx_len: np.ndarray,
     return dict(k=k, v=v, cap=cap, base=base)
 
 
-def make_weights(cfg: Config, seed: int = 0, with_embed: bool = True) -> Dict[str, np.ndarray]:
+def make_weights(cfg: Config, seed: int = 0, with_embed: bool = True, layer: int = 0) -> Dict[str, np.ndarray]:
     """Layer + LM-head weights as raw bf16 bits, PyTorch Linear layout [out][in].
 
     Linear/embedding weights ~ N(0, std^2) (std 0.02); norm gains are 1.0.
     The MoE router uses std 1/sqrt(hidden) so its logits are about N(0, 1)
-    on unit-RMS inputs."""
+    on unit-RMS inputs.  Decoder layer `layer` > 0 draws its layer weights
+    from streams of its own and carries no embedding, final norm or LM head."""
+    if layer > 0:
+        return _layer_weights(cfg, seed, layer)
     ly = cfg.layer
     H, hd = ly.hidden, ly.head_dim
     s = cfg.weight_std
@@ -246,6 +251,28 @@ def make_weights(cfg: Config, seed: int = 0, with_embed: bool = True) -> Dict[st
         w["w_exp_down"] = _normal_bf16(seed, cfg.cid, "w_exp_down", E * H * Ie, s).reshape(E, H, Ie)
     w["final_norm"] = np.full(H, BF16_ONE, dtype=np.uint16)
     w["w_lm"] = _normal_bf16(seed, cfg.cid, "w_lm", ly.vocab * H, s).reshape(ly.vocab, H)
+    return w
+
+
+def _layer_weights(cfg: Config, seed: int, layer: int) -> Dict[str, np.ndarray]:
+    ly = cfg.layer
+    H, hd = ly.hidden, ly.head_dim
+    s = cfg.weight_std
+    nqkv = (ly.n_q + 2 * ly.n_kv) * hd
+    nb = lambda tag, n, std: _normal_bf16(seed, cfg.cid, tag, n, std, layer=layer)
+    w: Dict[str, np.ndarray] = {}
+    w["attn_norm"] = np.full(H, BF16_ONE, dtype=np.uint16)
+    w["w_qkv"] = nb("w_qkv", nqkv * H, s).reshape(nqkv, H)
+    w["w_o"] = nb("w_o", H * ly.n_q * hd, s).reshape(H, ly.n_q * hd)
+    w["mlp_norm"] = np.full(H, BF16_ONE, dtype=np.uint16)
+    if ly.n_exp == 0:
+        w["w_gate_up"] = nb("w_gate_up", 2 * ly.inter * H, s).reshape(2 * ly.inter, H)
+        w["w_down"] = nb("w_down", H * ly.inter, s).reshape(H, ly.inter)
+    else:
+        E, Ie = ly.n_exp, ly.exp_inter
+        w["w_router"] = nb("w_router", E * H, 1.0 / math.sqrt(H)).reshape(E, H)
+        w["w_exp_gate_up"] = nb("w_exp_gate_up", E * 2 * Ie * H, s).reshape(E, 2 * Ie, H)
+        w["w_exp_down"] = nb("w_exp_down", E * H * Ie, s).reshape(E, H, Ie)
     return w
 
 
