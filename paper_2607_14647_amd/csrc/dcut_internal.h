@@ -102,7 +102,7 @@ struct GemmArgs {
   int n_q, n_kv, head_dim;
   // EPI_ARGMAX
   unsigned long long *amax_keys;  // [M_max][amax_slots]: per-row maxima of column ranges
-  int amax_slots;                 // row stride of amax_keys, at least gemm_argmax_slots()
+  int amax_slots;                 // row stride of amax_keys, at least both gemm_argmax_slots() counts
   // EPI_SAMPLE: noise of column c at row t is keyed by (seed, row_req[t], row_pos[t], c)
   float inv_temp;
   uint32_t seed_lo, seed_hi;
@@ -127,7 +127,15 @@ struct GemmArgs {
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s);
 // number of per-row partial argmax keys EPI_ARGMAX writes for this shape (at most 2 * ceil(N / 128))
-int gemm_argmax_slots(const GemmArgs &a);
+// The LM-head GEMM with the argmax epilogue takes its tile on the device from
+// the live row count M: 128 x 256 tiles with a four-slice W ring when the last
+// 256-row tile would be at most half full, 256 x 256 tiles otherwise.  Both
+// give bitwise the same results.
+__host__ __device__ inline bool lm_head_mid_tile(int M) { return M > 0 && M % 256 != 0 && M % 256 <= 128; }
+// Partial-key slots per row the argmax/sample GEMM writes: *big when the live
+// rows take the 256 x 256 tile, *mid when they take the 128 x 256 one (equal
+// when the launch makes no such choice).  The row stride must hold the larger.
+void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid);
 // split-K factor for a residual GEMM of this shape (a function of M_max, never of K*)
 int gemm_splits(int M_max, int N, int K);
 

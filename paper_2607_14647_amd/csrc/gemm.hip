@@ -46,18 +46,20 @@ constexpr int TK = 64;       // k per LDS stage: one 128-byte row per operand ro
 constexpr int CPR = TK / 8;  // 16-byte chunks per row
 constexpr int RPI = 64 / CPR;  // rows per 1 KB wave load
 
-template <int GM_, int GN_, int WM_, int WN_>
+template <int GM_, int GN_, int WM_, int WN_, int NA_ = 2, int NB_ = 3>
 struct Tile {
   static constexpr int GM = GM_, GN = GN_, WM = WM_, WN = WN_;
   static constexpr int NWV = GM * GN, THREADS = 64 * NWV;
   static constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
-  static constexpr int NA = 2, NB = 3;   // ring stages of A and W
+  static constexpr int NA = NA_, NB = NB_;   // ring stages of A and W (NA = 2, NB = 3 or 4)
+  static_assert(NA == 2 && (NB == 3 || NB == 4), "ring depths the wait counts are written for");
   static constexpr size_t LDS = (size_t)(NA * TM + NB * TN) * TK * sizeof(uint16_t);
   static constexpr int PER_CU = LDS > 81920 ? 1 : 2;
 };
 using Big = Tile<4, 2, 2, 4>;
 using Mid = Tile<2, 4, 2, 2>;     // 128 x 256, eight waves in a 2 x 4 grid, 128 KB
 using Small = Tile<2, 2, 2, 2>;
+using MidDeep = Tile<2, 4, 2, 2, 2, 4>;   // 128 x 256 with four W slices: the LM head at few live rows
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -267,16 +269,33 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
 
     const int kt0 = sp * per_split;
     const int nk = max(0, min(nk_all, kt0 + per_split) - kt0);
-    // prologue: A slice 0, W slices 0 and 1
+    constexpr int PW = NB - 1;     // W slices in flight ahead of the one multiplied
+    // prologue: A slice 0, W slices 0 .. PW-1
     if (nk > 0) {
       issueA(kt0, 0);
       issueW(kt0, 0);
     }
-    if (nk > 1) issueW(kt0 + 1, 1);
+#pragma unroll
+    for (int p = 1; p < PW; ++p)
+      if (p < nk) issueW(kt0 + p, p);
     for (int it = 0; it < nk; ++it) {
-      // outstanding, oldest first: ..., W[it], A[it], W[it+1] (when it exists)
-      if (it + 1 < nk) wait_vm<BJ>();
-      else wait_vm<0>();
+      // issue order: A[0] W[0] .. W[PW-1], then per iteration A[it+1] W[it+PW].
+      // A[it] and W[it] are done once at most the W slices issued after A[it]
+      // remain: W[1 .. PW-1] at it = 0, W[it+PW-1] later (when they exist)
+      if constexpr (PW == 2) {
+        if (it + 1 < nk) wait_vm<BJ>();
+        else wait_vm<0>();
+      } else {                     // PW == 3
+        if (it == 0) {
+          if (nk > 2) wait_vm<2 * BJ>();
+          else if (nk == 2) wait_vm<BJ>();
+          else wait_vm<0>();
+        } else if (it + 2 < nk) {
+          wait_vm<BJ>();
+        } else {
+          wait_vm<0>();
+        }
+      }
       ring_barrier();
       const uint16_t *sa = ldsA + (it % NA) * (TM * TK);
       const uint16_t *sb = ldsW + (it % NB) * (TN * TK);
@@ -287,7 +306,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
 #pragma unroll
       for (int j = 0; j < WN; ++j) fb[0][j] = *(const bf16x8 *)(sb + bfrag[j] + 8 * (kh ^ brx[j]));
       if (it + 1 < nk) issueA(kt0 + it + 1, (it + 1) % NA);
-      if (it + 2 < nk) issueW(kt0 + it + 2, (it + 2) % NB);
+      if (it + PW < nk) issueW(kt0 + it + PW, (it + PW) % NB);
 #pragma unroll
       for (int ks = 0; ks < TK / 16; ++ks) {
         const int cur = ks & 1;
@@ -541,10 +560,16 @@ template <int EPI>
 __global__ void __launch_bounds__(Big::THREADS)
 k_gemm_dual(GemmArgs a) {
   static_assert(Mid::THREADS == Big::THREADS && Mid::LDS <= Big::LDS, "one launch shape for both tiles");
+  static_assert(MidDeep::THREADS == Big::THREADS && MidDeep::LDS <= Big::LDS, "one launch shape for both tiles");
   const int M = *a.m_count;
-  const long long big_tasks = (long long)((M + Big::TM - 1) / Big::TM) * n_col_tiles<EPI>(a, Big::TN);
-  if (4 * big_tasks < 3LL * gridDim.x) gemm_tasks<EPI, Mid>(a);
-  else gemm_tasks<EPI, Big>(a);
+  if constexpr (EPI == EPI_SWIGLU) {
+    const long long big_tasks = (long long)((M + Big::TM - 1) / Big::TM) * n_col_tiles<EPI>(a, Big::TN);
+    if (4 * big_tasks < 3LL * gridDim.x) gemm_tasks<EPI, Mid>(a);
+    else gemm_tasks<EPI, Big>(a);
+  } else {
+    if (lm_head_mid_tile(M)) gemm_tasks<EPI, MidDeep>(a);
+    else gemm_tasks<EPI, Big>(a);
+  }
 }
 
 // out[m][n] (+)= sum over splits of part[s][m][n], in split order (rows m < K*).
@@ -632,7 +657,8 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
 }
 
 // Big tiles for dense GEMMs with at least one Big tile per CU at M_max rows
-// (the SwiGLU GEMM picks Big or Mid on the device from the live rows); Small
+// (the SwiGLU and LM-head GEMMs pick Big or a 128-row tile on the device from
+// the live rows); Small
 // tiles for the others, for grouped (MoE row tiles of 128) and for split-K
 // GEMMs.
 template <int EPI>
@@ -641,8 +667,11 @@ int launch_epi(int kid, const GemmArgs &a, hipStream_t s) {
   const long long big_tasks = (long long)((a.M_max + Big::TM - 1) / Big::TM) *
       (EPI == EPI_SWIGLU ? (a.swiglu_inter + Big::TN / 2 - 1) / (Big::TN / 2) : (a.N + Big::TN - 1) / Big::TN);
   if (big_tasks < cu_count()) return launch_tile<EPI, Small>(kid, a, s);
-  if constexpr (EPI == EPI_SWIGLU) {
-    // tile shape chosen on the device from the live row count (one workgroup per CU)
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_ARGMAX) {
+    // tile shape chosen on the device from the live row count (one workgroup per CU);
+    // the sampling epilogue keeps the 256-row tile (both paths in one kernel would spill)
+    if (EPI == EPI_ARGMAX && (!a.amax_keys || a.amax_slots < (a.N + MidDeep::TN - 1) / MidDeep::TN * MidDeep::GN))
+      return DCUT_EINVAL;
     const int g = (cu_count() + 7) / 8 * 8;
     return launch(kid, k_gemm_dual<EPI>, dim3((unsigned)g), dim3(Big::THREADS), Big::LDS, s, a);
   } else {
@@ -662,10 +691,15 @@ int gemm_splits(int M_max, int N, int K) {
   return sp < 1 ? 1 : sp;
 }
 
-int gemm_argmax_slots(const GemmArgs &a) {
-  const bool big = !a.tiles && a.splits <= 1 &&
-                   (long long)((a.M_max + Big::TM - 1) / Big::TM) * ((a.N + Big::TN - 1) / Big::TN) >= cu_count();
-  return big ? (a.N + Big::TN - 1) / Big::TN * Big::GN : (a.N + Small::TN - 1) / Small::TN * Small::GN;
+void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid) {
+  const bool big_tiles = !a.tiles && a.splits <= 1 &&
+                         (long long)((a.M_max + Big::TM - 1) / Big::TM) * ((a.N + Big::TN - 1) / Big::TN) >= cu_count();
+  if (big_tiles) {
+    *big = (a.N + Big::TN - 1) / Big::TN * Big::GN;
+    *mid = epi == EPI_ARGMAX ? (a.N + MidDeep::TN - 1) / MidDeep::TN * MidDeep::GN : *big;
+  } else {
+    *big = *mid = (a.N + Small::TN - 1) / Small::TN * Small::GN;
+  }
 }
 
 int gemm_launch(int kid, EpiKind epi, const GemmArgs &a, hipStream_t s) {

@@ -15,7 +15,7 @@ namespace dcut {
 
 size_t lmhead_ws_bytes(int H, int V, int B, int D) {
   const size_t M = (size_t)B * (D + 1);
-  const size_t slots = 2 * (((size_t)V + 127) / 128);   // row stride of the partial keys
+  const size_t slots = 4 * (((size_t)V + 255) / 256);   // row stride of the partial keys (64 columns each)
   // normalised rows, partial keys, partial log-partition pairs
   return align256(M * H * 2) + 2 * align256(M * slots * sizeof(unsigned long long));
 }
@@ -33,13 +33,15 @@ __device__ __forceinline__ void lse_merge(float &m, float &s, float m2, float s2
 }
 
 __global__ void __launch_bounds__(256)
-k_argmax_final(const unsigned long long *__restrict__ keys, const float2 *__restrict__ part, int slots,
-               int stride, const int32_t *__restrict__ m_count, int M_max, int32_t *__restrict__ argmax,
-               float *__restrict__ max_logit, float *__restrict__ lse) {
+k_argmax_final(const unsigned long long *__restrict__ keys, const float2 *__restrict__ part, int slots_big,
+               int slots_mid, int stride, const int32_t *__restrict__ m_count, int M_max,
+               int32_t *__restrict__ argmax, float *__restrict__ max_logit, float *__restrict__ lse) {
   __shared__ unsigned long long s_max[4];
   __shared__ float s_m[4], s_s[4];
   const int t = blockIdx.x;
-  if (t >= M_max || t >= *m_count) return;
+  const int M = *m_count;
+  if (t >= M_max || t >= M) return;
+  const int slots = lm_head_mid_tile(M) ? slots_mid : slots_big;   // the GEMM's own tile choice
   const int tid = threadIdx.x, lane = tid & 63;
   const unsigned long long *row = keys + (size_t)t * stride;
   unsigned long long k = 0ull;
@@ -98,7 +100,7 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
   uint16_t *f = (uint16_t *)ws;
-  const int slots = 2 * ((V + 127) / 128);   // row stride; the GEMM writes gemm_argmax_slots() of them
+  const int slots = 4 * ((V + 255) / 256);   // row stride; holds either of the gemm_argmax_slots() counts
   unsigned long long *keys = (unsigned long long *)((char *)ws + align256((size_t)M * H * 2));
   float2 *part = (float2 *)((char *)keys + align256((size_t)M * slots * sizeof(unsigned long long)));
   const int32_t *Kstar = cu + B;
@@ -111,11 +113,12 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   g.row_req = row_req; g.row_pos = row_pos; g.inv_temp = inv_temp;
   g.lse_part = lse ? part : nullptr;
   g.seed_lo = (uint32_t)seed; g.seed_hi = (uint32_t)(seed >> 32);
-  const int used = gemm_argmax_slots(g);
+  int used_big, used_mid;
+  gemm_argmax_slots(g, epi, &used_big, &used_mid);
   DCUT_TRY(gemm_launch(DCUT_KERNEL_LM_HEAD, epi, g, stream));
   return launch(DCUT_KERNEL_ARGMAX_FINAL, k_argmax_final, dim3(M), dim3(256), 0, stream,
-                (const unsigned long long *)keys, (const float2 *)part, used, slots, Kstar, M, token,
-                max_score, lse);
+                (const unsigned long long *)keys, (const float2 *)part, used_big, used_mid, slots, Kstar, M,
+                token, max_score, lse);
 }
 
 extern "C" int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,

@@ -64,7 +64,9 @@ def test_workspace_sizes():
     assert 0 < ws1 < (1 << 31) and ws1 % 256 == 0
     # normalised rows plus, per row and 64 columns of the vocabulary, one key and one
     # (max, sum) pair of the log-partition function
-    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 2 * 1024 * 2 * ((cfg.vocab + 127) // 128) * 8
+    assert L.workspace_bytes(2, cfg, 64, 15) >= 1024 * 4096 * 2 + 2 * 1024 * 4 * ((cfg.vocab + 255) // 256) * 8
+    odd = L.LayerCfg(2048, 32, 4, 128, 0, 128, 8, 768, 151936, 4112, 1e-5, 1e6)      # V / 128 odd
+    assert L.workspace_bytes(2, odd, 128, 15) >= 2048 * 2048 * 2 + 2 * 2048 * 4 * ((151936 + 255) // 256) * 8
     # RS acceptance: two int32 per request plus one key per request and 2048-column chunk
     nch = (cfg.vocab + 2047) // 2048
     assert L.workspace_bytes(4, cfg, 64, 15) >= 64 * 8 + 64 * nch * 8

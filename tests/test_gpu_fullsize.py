@@ -72,6 +72,8 @@ def test_fullsize_sampled_requests(cid):
             rows_f.append(int(np.where(rows == sel["cu"][i] + k)[0][0]))
     lg_p = logits[torch.tensor(rows_p, device="cuda")].cpu().numpy()
     assert np.array_equal(lg_p, lg_gpu[rows_f]), "logits changed with the budget"
+    # the argmax too, whichever LM-head tile each live row count takes
+    assert np.array_equal(vs.host("argmax")[rows_p], am_gpu[rows_f]), "argmax changed with the budget"
     del logits
     note(f"cfg{cid}: oracle on requests {sample} ({len(rows)} rows)")
     w64 = olay.prepare_weights(w)
