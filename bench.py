@@ -261,7 +261,7 @@ def main():
     adaptive = lambda: run_step(budgets, cost_ms)
 
     # 4. per-kernel breakdown with the timing hook
-    names = ["SELECT", "PACK", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP",
+    names = ["SELECT", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP",
              "GEMM_DOWN", "LM_HEAD", "ARGMAX_FINAL"]
     names += ["RS_DECIDE", "RS_RESIDUAL", "RS_FINISH"] if args.rs else ["ACCEPT"]
     breakdown = {} if state is None else state["kernel_us"]

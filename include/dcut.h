@@ -351,7 +351,8 @@ int dcut_nearest_batch(int B, int n, const int32_t *captured);
  * calling thread: its next launches on this thread record `start` before and
  * `stop` after the kernel on the launch stream.  DCUT_KERNEL_NONE disarms. */
 enum {
-  DCUT_KERNEL_NONE = 0, DCUT_KERNEL_SELECT, DCUT_KERNEL_PACK, DCUT_KERNEL_NORM,
+  DCUT_KERNEL_NONE = 0, DCUT_KERNEL_SELECT /* selection and packing */,
+  DCUT_KERNEL_PACK /* no kernel of its own: packing runs in the selection kernel */, DCUT_KERNEL_NORM,
   DCUT_KERNEL_GEMM_QKV, DCUT_KERNEL_ATTN, DCUT_KERNEL_ATTN_COMBINE, DCUT_KERNEL_GEMM_O,
   DCUT_KERNEL_GEMM_GATE_UP, DCUT_KERNEL_GEMM_DOWN, DCUT_KERNEL_MOE, DCUT_KERNEL_LM_HEAD,
   DCUT_KERNEL_ARGMAX_FINAL, DCUT_KERNEL_ACCEPT, DCUT_KERNEL_RS_DECIDE, DCUT_KERNEL_RS_RESIDUAL,

@@ -4,9 +4,9 @@
 // packing of App. C; for rejection-sampling verification (App. B) the same
 // kernel ranks the shifted scores of Eq. dcut-shifted-score and chooses the
 // budget causally: by the early-stopping scan, or as a budget fixed beforehand.
-// Both kernels run as one 1024-thread workgroup: the whole problem is at most
-// 8192 positions (64 KB of sort keys in LDS), so a single
-// workgroup avoids any grid-wide synchronisation and launch round trips.
+// One 1024-thread workgroup does it all, packing included: the whole problem is
+// at most 8192 positions (64 KB of sort keys in LDS), so a single workgroup
+// avoids any grid-wide synchronisation and launch round trips.
 //
 // Bit-exactness: each request's scores are one sequential float32 product per
 // depth (denormals kept, no contraction); ranking uses the unique 64-bit key
@@ -63,7 +63,9 @@ __device__ __forceinline__ double objective(unsigned long long P, double cost) {
 }
 
 __global__ void __launch_bounds__(1024)
-k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ keep_len,
+k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restrict__ draft,
+         const int32_t *__restrict__ ctx_len, int32_t *__restrict__ keep_len, int32_t *__restrict__ cu,
+         int32_t *__restrict__ ptok, int32_t *__restrict__ ppos, int32_t *__restrict__ preq,
          int32_t *__restrict__ choice, unsigned long long *__restrict__ benefit,
          int32_t *__restrict__ dev_err, int32_t *__restrict__ k_state) {
   extern __shared__ unsigned long long smem[];
@@ -78,6 +80,9 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
   int NP = 64;
   while (NP < N) NP <<= 1;
   unsigned long long *keys = smem;          // [NP]
+  int *s_kl = (int *)smem;                  // [B], then s_cu [B+1]: the key area (and the prefix
+                                            // sums after it) once both are dead
+  int *s_cu = s_kl + B;
   float *s_conf = (float *)(smem + NP + blockDim.x);   // [B * D], staged once (coalesced)
   if (tid == 0) {
     s_err = 0;
@@ -238,49 +243,42 @@ k_select(SelectParams p, const float *__restrict__ conf, int32_t *__restrict__ k
     }
     if (rank_key(1.0f, 0, i) < tau) n = 0;   // impossible when K* >= B; kept for safety
     keep_len[i] = n;
+    s_kl[i] = n;
   }
-}
-#pragma clang fp contract(on)
+  __syncthreads();
 
-// Packing: cu = exclusive scan of keep_len; row t = cu[i] + k gets (z_{i,k}, L_i + k, i).
-__global__ void __launch_bounds__(1024)
-k_pack(int B, int D, const int32_t *__restrict__ keep_len, const int32_t *__restrict__ draft,
-       const int32_t *__restrict__ ctx_len, int32_t *__restrict__ cu, int32_t *__restrict__ ptok,
-       int32_t *__restrict__ ppos, int32_t *__restrict__ preq) {
-  __shared__ int s_cu[DCUT_MAX_BATCH + 1];
-  __shared__ int s_wave[17];
-  const int tid = threadIdx.x;
-  const int D1 = D + 1;
+  // 6. packing (App. C): cu = exclusive scan of keep_len; row t = cu[i] + k
+  // gets (z_{i,k}, L_i + k, i).  The sort keys are dead by now; their LDS holds
+  // the offsets.
   const int per = (B + blockDim.x - 1) / blockDim.x;   // <= 4
   int v[4];
-  int local = 0;
+  int loc = 0;
   for (int j = 0; j < per; ++j) {
-    int i = tid * per + j;
-    int kl = i < B ? keep_len[i] : 0;
-    kl = kl < 0 ? 0 : (kl > D1 ? D1 : kl);
-    v[j] = kl;
-    local += kl;
+    const int i = tid * per + j;
+    v[j] = i < B ? s_kl[i] : 0;
+    loc += v[j];
   }
-  int total;
-  int pre = block_exclusive_scan(local, s_wave, &total);
+  int kept;
+  int off = block_exclusive_scan(loc, (int *)s_wave, &kept);
   for (int j = 0; j < per; ++j) {
-    int i = tid * per + j;
-    if (i < B) s_cu[i] = pre;
-    pre += v[j];
+    const int i = tid * per + j;
+    if (i < B) s_cu[i] = off;
+    off += v[j];
   }
-  if (tid == 0) s_cu[B] = total;
+  if (tid == 0) s_cu[B] = kept;
   __syncthreads();
   for (int i = tid; i <= B; i += blockDim.x) cu[i] = s_cu[i];
-  for (int idx = tid; idx < B * D1; idx += blockDim.x) {
-    int i = idx / D1, k = idx - i * D1;
+  for (int idx = tid; idx < N; idx += blockDim.x) {
+    const int i = idx / D1, k = idx - i * D1;
     if (k < s_cu[i + 1] - s_cu[i]) {
-      int t = s_cu[i] + k;
+      const int t = s_cu[i] + k;
       ptok[t] = draft[idx];
       ppos[t] = ctx_len[i] + k;
       preq[t] = i;
     }
   }
 }
+#pragma clang fp contract(on)
 
 }  // namespace dcut
 
@@ -316,11 +314,9 @@ static int select_run(int B, int D, const float *conf, const int32_t *draft, con
   int N = B * (D + 1), NP = 64;
   while (NP < N) NP <<= 1;
   size_t shmem = (size_t)(NP + 1024) * sizeof(unsigned long long) + (size_t)B * D * sizeof(float);
-  DCUT_TRY(launch(DCUT_KERNEL_SELECT, k_select, dim3(1), dim3(1024), shmem, stream, p, conf,
-                  keep_len, choice, (unsigned long long *)benefit, dev_err, k_state));
-  DCUT_TRY(launch(DCUT_KERNEL_PACK, k_pack, dim3(1), dim3(1024), 0, stream, B, D,
-                  (const int32_t *)keep_len, draft, ctx_len, cu, packed_tok, packed_pos, packed_req));
-  return DCUT_OK;
+  return launch(DCUT_KERNEL_SELECT, k_select, dim3(1), dim3(1024), shmem, stream, p, conf, draft, ctx_len,
+                keep_len, cu, packed_tok, packed_pos, packed_req, choice, (unsigned long long *)benefit, dev_err,
+                k_state);
 }
 
 extern "C" int dcut_select(int B, int D, const float *conf, const int32_t *draft,

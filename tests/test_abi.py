@@ -31,7 +31,7 @@ def test_enums_match_header():
     for name, val in [("DCUT_EINVAL", L.EINVAL), ("DCUT_EWORKSPACE", L.EWORKSPACE),
                       ("DCUT_DERR_CAPACITY", L.DERR_CAPACITY)]:
         assert re.search(rf"{name}\s*=\s*{val}\b", src)
-    ids = re.search(r"DCUT_KERNEL_NONE = 0,([^}]*)\}", src).group(1)
+    ids = re.sub(r"/\*.*?\*/", "", re.search(r"DCUT_KERNEL_NONE = 0,([^}]*)\}", src).group(1), flags=re.S)
     names = ["NONE"] + [s.strip().replace("DCUT_KERNEL_", "") for s in ids.split(",") if s.strip()]
     assert names == list(L.KERNELS)
 
