@@ -45,15 +45,20 @@ __device__ __forceinline__ bool conf_bad(float c) { return !(c >= 0.0f && c <= 1
 // Step cost at an arbitrary verification size K for the causal scan: linear
 // between consecutive budgets (K_r, C_r), the end costs outside them, and the
 // last of several equal budgets at that K.  Same float64 operations, in the
-// same order, on every platform.
-__device__ double cost_at(const SelectParams &p, int K) {
-  int r = -1;
-  for (int t = 0; t < p.R; ++t)
-    if (p.budgets[t] <= K) r = t;
-  if (r < 0) return p.costs[0];
-  if (r == p.R - 1) return p.costs[p.R - 1];
-  const int ka = p.budgets[r], kb = p.budgets[r + 1];
-  const double ca = p.costs[r], cb = p.costs[r + 1];
+// same order, on every platform.  The candidates sit in LDS (bud, cst); r is
+// found by binary search over the non-decreasing budgets.
+__device__ double cost_at(const int *bud, const double *cst, int R, int K) {
+  int lo = 0, hi = R;                 // r = (number of budgets <= K) - 1
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (bud[mid] <= K) lo = mid + 1;
+    else hi = mid;
+  }
+  const int r = lo - 1;
+  if (r < 0) return cst[0];
+  if (r == R - 1) return cst[R - 1];
+  const int ka = bud[r], kb = bud[r + 1];
+  const double ca = cst[r], cb = cst[r + 1];
   return ca + ((cb - ca) * (double)(K - ka)) / (double)(kb - ka);
 }
 
@@ -71,6 +76,8 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
   extern __shared__ unsigned long long smem[];
   __shared__ unsigned long long s_wave[17];
   __shared__ unsigned long long s_ben[DCUT_MAX_CANDIDATES];
+  __shared__ double s_cost[DCUT_MAX_CANDIDATES], s_obj[DCUT_MAX_CANDIDATES];
+  __shared__ int s_bud[DCUT_MAX_CANDIDATES];
   __shared__ unsigned long long s_tau;
   __shared__ int s_err, s_stop;
 
@@ -89,6 +96,10 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
     s_stop = N;
   }
   for (int j = tid; j < B * D; j += blockDim.x) s_conf[j] = conf[j];
+  if (tid < p.R) {
+    s_bud[tid] = p.budgets[tid];
+    s_cost[tid] = p.costs[tid];
+  }
   __syncthreads();
 
   // 1. scores and keys, one thread per request, sequential in depth
@@ -108,45 +119,58 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
   }
   for (int j = N + tid; j < NP; j += blockDim.x) keys[j] = 0ull;   // sorts last
 
-  // 2. bitonic sort, descending
-  if (NP <= (int)blockDim.x) {
-    // one key per thread: compare-exchange partners closer than a wave apart
-    // swap through cross-lane shuffles (no barrier), farther ones through LDS
-    __syncthreads();
-    const bool act = tid < NP;               // whole waves (NP is a multiple of 64)
-    unsigned long long x = act ? keys[tid] : 0ull;
-    for (int size = 2; size <= NP; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        unsigned long long y;
-        if (stride >= 64) {
-          __syncthreads();
-          if (act) keys[tid] = x;
-          __syncthreads();
-          y = act ? keys[tid ^ stride] : 0ull;
-        } else {
-          y = __shfl_xor(x, stride, 64);
+  // 2. sort, descending.  Each wave sorts 64-key runs in registers (a bitonic
+  // network over cross-lane shuffles, no barrier); then runs are merged
+  // pairwise: a key's place in the merged run is its index in its own run plus
+  // the number of keys ahead of it in the other run (a binary search; equal
+  // keys, which only the zero padding has, go left run first).
+  __syncthreads();
+  {
+    const int lane = tid & 63, wv = tid >> 6, nwv = blockDim.x >> 6;
+    for (int run = wv; run < NP / 64; run += nwv) {
+      unsigned long long x = keys[run * 64 + lane];
+#pragma unroll
+      for (int size = 2; size <= 64; size <<= 1)
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+          const unsigned long long y = __shfl_xor(x, stride, 64);
+          // the lower lane of a pair keeps the larger key in a descending run
+          const bool take_max = ((lane & stride) == 0) == ((lane & size) == 0);
+          x = take_max ? (x > y ? x : y) : (x < y ? x : y);
         }
-        // the lower index of a pair keeps the larger key in a descending run
-        const bool take_max = ((tid & stride) == 0) == ((tid & size) == 0);
-        x = take_max ? (x > y ? x : y) : (x < y ? x : y);
-      }
+      keys[run * 64 + lane] = x;
     }
-    __syncthreads();
-    if (act) keys[tid] = x;
-  } else {
-    for (int size = 2; size <= NP; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        __syncthreads();
-        for (int t = tid; t < (NP >> 1); t += blockDim.x) {
-          int lo = 2 * t - (t & (stride - 1));
-          int hi = lo + stride;
-          unsigned long long a = keys[lo], b = keys[hi];
-          bool desc = (lo & size) == 0;
-          if (desc ? (a < b) : (a > b)) {
-            keys[lo] = b;
-            keys[hi] = a;
-          }
+    const int EM = NP > (int)blockDim.x ? NP / (int)blockDim.x : 1;   // keys per thread, <= 8
+    for (int width = 64; width < NP; width <<= 1) {
+      __syncthreads();
+      unsigned long long mine[8];
+      int dest[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (e >= EM) break;
+        const int idx = tid + e * (int)blockDim.x;
+        dest[e] = -1;
+        if (idx >= NP) continue;
+        const unsigned long long x = keys[idx];
+        const int base = idx & ~(2 * width - 1);
+        const bool left = idx - base < width;
+        const int own = idx - base - (left ? 0 : width);
+        const unsigned long long *other = keys + base + (left ? width : 0);
+        int lo = 0, hi = width;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          const unsigned long long o = other[mid];
+          if (left ? (o > x) : (o >= x)) lo = mid + 1;
+          else hi = mid;
         }
+        mine[e] = x;
+        dest[e] = base + own + lo;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (e >= EM) break;
+        if (dest[e] >= 0) keys[dest[e]] = mine[e];
       }
     }
   }
@@ -168,6 +192,7 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
     unsigned long long P = (t < (int)blockDim.x) ? s_pre[t] : total;
     for (int m = t * E; m < t * E + rem; ++m) P += key_units(keys[m]);
     s_ben[tid] = P;
+    s_obj[tid] = objective(P, s_cost[tid]);   // every candidate's objective at once
     if (benefit) benefit[tid] = P;
   }
   __syncthreads();
@@ -180,7 +205,8 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
     int stop = N;
     for (int m = tid * E; m < tid * E + E && m < N; ++m) {
       const unsigned long long P1 = P + key_units(keys[m]);
-      if (m >= B && !(objective(P1, cost_at(p, m + 1)) > objective(P, cost_at(p, m)))) {
+      if (m >= B && !(objective(P1, cost_at(s_bud, s_cost, p.R, m + 1)) >
+                      objective(P, cost_at(s_bud, s_cost, p.R, m)))) {
         stop = m;
         break;
       }
@@ -198,7 +224,7 @@ k_select(SelectParams p, const float *__restrict__ conf, const int32_t *__restri
     int bucket = 0;                   // first strict maximum of the objective over the candidates
     double best_obj = -1.0;
     for (int r = 0; r < p.R; ++r) {
-      double obj = objective(s_ben[r], p.costs[r]);
+      const double obj = s_obj[r];
       if (obj > best_obj) {
         best_obj = obj;
         bucket = r;
