@@ -114,6 +114,7 @@ struct GemmArgs {
   // split-K (EPI_RESID_F32 / EPI_STORE_F32): partial tiles [splits][M_max][N] float32
   int splits;
   float *split_part;
+  int defer_reduce;               // with splits > 1: leave the partials for the caller to add
   // grouped mode (MoE experts): row tiles come from a device list of
   // (expert, first row, end row); W advances by w_stride elements per expert;
   // A rows are gathered through a_rows when it is not null.
@@ -140,6 +141,11 @@ void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid);
 int gemm_splits(int M_max, int N, int K);
 
 // ---------------------------------------------------------------- other launchers
+// x[m] += sum of the split-K partials part[s][m] (in split order), then
+// h[m] = RMSNorm(x[m]) * gain: the residual add of a split-K GEMM fused with the
+// norm that reads its result.  One workgroup per live row; H % 8 == 0, H <= 8192.
+int reduce_rmsnorm_launch(int kid, const float *part, int splits, int M_max, int H, const int32_t *m_count,
+                          float *x, const uint16_t *gain, float eps, uint16_t *h_out, hipStream_t s);
 int rmsnorm_launch(int kid, const float *x_in, const uint16_t *embed, const int32_t *tok, int vocab,
                    const uint16_t *gain, float eps, int H, int M_max, const int32_t *m_count,
                    float *x_copy, uint16_t *h_out, const int32_t *pos, int head_dim, float theta,

@@ -645,6 +645,7 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   g = (g + 7) / 8 * 8;
   if (g < 8) g = 8;
   DCUT_TRY(launch(kid, k_gemm<EPI, T>, dim3((unsigned)g), dim3(T::THREADS), T::LDS, s, a));
+  if (splits > 1 && a.defer_reduce) return DCUT_OK;
   if (splits > 1 && EPI == EPI_QKV_ROPE) {
     const int pairs = (a.n_q + 2 * a.n_kv) * (a.head_dim / 2);
     return launch(DCUT_KERNEL_NONE, k_qkv_reduce, dim3((pairs + 255) / 256, a.M_max), dim3(256), 0, s, a);

@@ -143,10 +143,16 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   o.W = w->w_o; o.ldw = nq * hd; o.N = H;
   o.out_f32 = x_out; o.ldo = H;
   o.splits = L.split_o; o.split_part = split;
+  // 5. norm2; with split-K, the residual add of the O projection is fused into it
+  const bool fuse = L.split_o > 1 && H <= 8192;
+  o.defer_reduce = fuse ? 1 : 0;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_O, EPI_RESID_F32, o, stream));
-  // 5. norm2
-  DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x_out, nullptr, nullptr, 0, w->mlp_norm, cfg->rms_eps, H,
-                          M, Kstar, nullptr, h, nullptr, 0, 0.0f, nullptr, nullptr, dev_err, stream));
+  if (fuse)
+    DCUT_TRY(reduce_rmsnorm_launch(DCUT_KERNEL_NORM, split, L.split_o, M, H, Kstar, x_out, w->mlp_norm,
+                                   cfg->rms_eps, h, stream));
+  else
+    DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x_out, nullptr, nullptr, 0, w->mlp_norm, cfg->rms_eps, H,
+                            M, Kstar, nullptr, h, nullptr, 0, 0.0f, nullptr, nullptr, dev_err, stream));
   // 6. MLP
   if (cfg->n_exp > 0) {
     MoeArgs me = {};

@@ -99,7 +99,70 @@ k_rmsnorm(const float *__restrict__ x_in, const uint16_t *__restrict__ embed,
   if (amax_init && tid == 0) amax_init[t] = 0ull;
 }
 
+// Split-K residual add and the following RMSNorm in one pass over the row.
+__global__ void __launch_bounds__(256)
+k_reduce_rmsnorm(const float *__restrict__ part, int splits, int M_max, int H,
+                 const int32_t *__restrict__ m_count, float *__restrict__ x, const uint16_t *__restrict__ gain,
+                 float eps, uint16_t *__restrict__ h_out) {
+  __shared__ float s_red[4];
+  const int t = blockIdx.x;
+  if (t >= *m_count) return;
+  const int tid = threadIdx.x;
+  const int ng = H / 8;
+  float v[4][8];                         // this thread's 8-element groups g = tid + 256 q
+  float ss = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int gi = tid + 256 * q;
+    if (gi >= ng) break;
+    const float *p0 = part + (size_t)t * H + gi * 8;
+    float4 a = *(const float4 *)p0, b = *(const float4 *)(p0 + 4);
+    for (int sp = 1; sp < splits; ++sp) {
+      const float *ps = part + ((size_t)sp * M_max + t) * H + gi * 8;
+      const float4 c = *(const float4 *)ps, d = *(const float4 *)(ps + 4);
+      a.x += c.x; a.y += c.y; a.z += c.z; a.w += c.w;
+      b.x += d.x; b.y += d.y; b.z += d.z; b.w += d.w;
+    }
+    float *xr = x + (size_t)t * H + gi * 8;
+    const float4 xa = *(const float4 *)xr, xb = *(const float4 *)(xr + 4);
+    a.x += xa.x; a.y += xa.y; a.z += xa.z; a.w += xa.w;
+    b.x += xb.x; b.y += xb.y; b.z += xb.z; b.w += xb.w;
+    *(float4 *)xr = a;
+    *(float4 *)(xr + 4) = b;
+    v[q][0] = a.x; v[q][1] = a.y; v[q][2] = a.z; v[q][3] = a.w;
+    v[q][4] = b.x; v[q][5] = b.y; v[q][6] = b.z; v[q][7] = b.w;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ss += v[q][j] * v[q][j];
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  if ((tid & 63) == 0) s_red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+  const float r = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int gi = tid + 256 * q;
+    if (gi >= ng) break;
+    uint4 gv = *(const uint4 *)(gain + gi * 8);
+    const uint16_t *gg = (const uint16_t *)&gv;
+    uint4 o;
+    uint32_t *ow = (uint32_t *)&o;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      ow[j] = pack_bf2(v[q][2 * j] * r * bf2f(gg[2 * j]), v[q][2 * j + 1] * r * bf2f(gg[2 * j + 1]));
+    *(uint4 *)(h_out + (size_t)t * H + gi * 8) = o;
+  }
+}
+
 }  // namespace
+
+int reduce_rmsnorm_launch(int kid, const float *part, int splits, int M_max, int H, const int32_t *m_count,
+                          float *x, const uint16_t *gain, float eps, uint16_t *h_out, hipStream_t s) {
+  if (H % 8 || H > 8 * 256 * 4 || splits < 1) return DCUT_EINVAL;
+  return launch(kid, k_reduce_rmsnorm, dim3(M_max), dim3(256), 0, s, part, splits, M_max, H, m_count, x, gain,
+                eps, h_out);
+}
 
 int rmsnorm_launch(int kid, const float *x_in, const uint16_t *embed, const int32_t *tok, int vocab,
                    const uint16_t *gain, float eps, int H, int M_max, const int32_t *m_count,
