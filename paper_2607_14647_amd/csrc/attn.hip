@@ -327,20 +327,43 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
   const int nc = n_chunks(L, a.chunk, MC);
   if (nc == 1) return;
   const float *pp = a.part + ((size_t)t * a.n_q + head) * MC * (HD + 2);
+  // the loads of up to CG chunks are issued together (one memory latency per
+  // group rather than per chunk); the sums still run in chunk order
+  constexpr int CG = 8;
   float mx = -__builtin_inff();
-  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, pp[c * (HD + 2) + HD]);
+  for (int c0 = 0; c0 < nc; c0 += CG) {
+    float mv[CG];
+#pragma unroll
+    for (int c = 0; c < CG; ++c) mv[c] = c0 + c < nc ? pp[(c0 + c) * (HD + 2) + HD] : -__builtin_inff();
+#pragma unroll
+    for (int c = 0; c < CG; ++c) mx = fmaxf(mx, mv[c]);
+  }
   constexpr int PER = HD / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
   float lsum = 0.0f;
-  for (int c = 0; c < nc; ++c) {
-    const float *q = pp + c * (HD + 2);
-    float mc = q[HD];
-    float sc = (mc == -__builtin_inff()) ? 0.0f : exp2f(mc - mx);
-    lsum += q[HD + 1] * sc;
+  for (int c0 = 0; c0 < nc; c0 += CG) {
+    float mv[CG], lv[CG], xv[CG][PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += q[lane * PER + e] * sc;
+    for (int c = 0; c < CG; ++c) {
+      if (c0 + c < nc) {
+        const float *q = pp + (c0 + c) * (HD + 2);
+        mv[c] = q[HD];
+        lv[c] = q[HD + 1];
+#pragma unroll
+        for (int e = 0; e < PER; ++e) xv[c][e] = q[lane * PER + e];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+      if (c0 + c < nc) {
+        const float sc = (mv[c] == -__builtin_inff()) ? 0.0f : exp2f(mv[c] - mx);
+        lsum += lv[c] * sc;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] += xv[c][e] * sc;
+      }
+    }
   }
   const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
   uint16_t *op = a.out + ((size_t)t * a.n_q + head) * HD;
