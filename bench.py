@@ -139,11 +139,17 @@ def cpu_baseline(cfg, st, w, kv, budgets, costs, target_s=15.0):
     log(f"cpu baseline: one request {dt1:.2f}s -> sample of {n} requests; forcing their drafts")
     z = odr.force_matches(ly, w64, kv, st["conf"], st["draft"], st["match_u"], st["ctx_len"], cfg.D,
                           requests=sample)
+    # the same pass repeated until about 10 s of CPU work have run (the whole batch may take less)
     dt, tokens, nrows = run(sample, z)
-    return dict(value=round(tokens / dt, 2), unit="accepted tokens/s", cores=int(cores), kind="oracle",
+    passes = 1
+    while dt < 10.0:
+        d2, _, _ = run(sample, z)
+        dt += d2
+        passes += 1
+    return dict(value=round(tokens * passes / dt, 2), unit="accepted tokens/s", cores=int(cores), kind="oracle",
                 sample=f"requests 0..{n - 1} of the batch ({nrows} kept rows, {tokens} accepted tokens): "
                        f"full-batch selection, then the float64 layer + LM head + accept for the sample; "
-                       f"{dt:.1f} s", seconds=round(dt, 2))
+                       f"{passes} passes, {dt:.1f} s", seconds=round(dt, 2))
 
 
 def main():
