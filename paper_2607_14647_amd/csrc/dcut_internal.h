@@ -35,10 +35,25 @@ struct ProfileHook {
 };
 ProfileHook &profile_hook();
 
-// Allow `kernel` to use `bytes` of dynamic LDS (needed above 64 KB); done once per kernel.
+// Allow `kernel` to use `bytes` of dynamic LDS (needed above 64 KB).  The
+// attribute is set once per kernel and size for each host thread (a small
+// per-thread table of what it set; setting it again from another thread is
+// harmless).
 template <typename Kernel>
 inline void allow_lds(Kernel kernel, size_t bytes) {
-  if (bytes > 65536) (void)hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (bytes <= 65536) return;
+  static thread_local const void *done_fn[64];
+  static thread_local size_t done_bytes[64];
+  static thread_local int n_done = 0;
+  const void *f = (const void *)kernel;
+  const int n = n_done < 64 ? n_done : 64;
+  for (int j = 0; j < n; ++j)
+    if (done_fn[j] == f && done_bytes[j] >= bytes) return;
+  if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) == hipSuccess && n_done < 64) {
+    done_fn[n_done] = f;
+    done_bytes[n_done] = bytes;
+    ++n_done;
+  }
 }
 
 // Launch `kernel`, recording the armed profiling events around it when `kid` is armed.
