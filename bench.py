@@ -174,6 +174,9 @@ def main():
                     help="rejection-sampling verification (dcut_select_rs with the causal scan, "
                          "dcut_lm_head_sample with logits, dcut_accept_rs) against a synthetic stochastic "
                          "drafter; temperature 1 unless --temperature is given")
+    ap.add_argument("--rs-budget", choices=("scan", "history"), default="scan",
+                    help="with --rs: the causal early-stopping scan over the cost row, or the history-based "
+                         "budget (the previous block's choice, carried on the device)")
     ap.add_argument("--layers", type=int, default=1,
                     help="decoder layers in the verify pass (each with its own seeded weights and KV cache); "
                          "32 is the full depth of the 8B-shaped target")
@@ -228,6 +231,8 @@ def main():
         assert state.get("layers", 1) == args.layers, "state mismatch (layers)"
     if args.rs:
         vs.enable_rs(None)
+        vs.rs_mode = L.RS_HISTORY if args.rs_budget == "history" else L.RS_SCAN
+        vs.k_state.fill_(budgets[-1])
         log("stochastic drafter: proposals and drafts from the target's own distributions (D passes)")
         runner.force_drafts_rs_on_device(vs, st["draft"], st["conf"], st["match_u"], args.sample_seed + 1000)
     elif state is not None:
@@ -405,8 +410,9 @@ def main():
                     layers=args.layers,
                     budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm",
                     target_decoding="greedy" if args.temperature == 0 else
-                    (f"rejection sampling at temperature {args.temperature} (causal scan over shifted "
-                     f"scores; seed {args.sample_seed})" if args.rs else
+                    (f"rejection sampling at temperature {args.temperature} ("
+                     + ("causal scan" if args.rs_budget == "scan" else "history-based budget")
+                     + f" over shifted scores; seed {args.sample_seed})" if args.rs else
                      f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})")),
         hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         step_algorithmic_bytes=int(step_bytes),
