@@ -68,7 +68,7 @@ extern "C" int dcut_nearest_batch(int B, int n, const int32_t *captured) {
 }
 
 extern "C" int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop) {
-  if (kernel < DCUT_KERNEL_NONE || kernel > DCUT_KERNEL_RS_FINISH) return DCUT_EINVAL;
+  if (kernel < DCUT_KERNEL_NONE || kernel > DCUT_KERNEL_ATTN_PLAN) return DCUT_EINVAL;
   if (kernel != DCUT_KERNEL_NONE && (!start || !stop)) return DCUT_EINVAL;
   ProfileHook &h = profile_hook();
   h.kernel = kernel;

@@ -189,7 +189,11 @@ struct AttnArgs {
   float *part;              // [M_max][n_q][max_chunks][hd + 2]
   uint16_t *out;            // [M][n_q][hd] bf16
   int32_t *dev_err;
+  int32_t *plan;            // work-order scratch of attn_plan_bytes(B, n_kv, max_chunks), or null
 };
+// Bytes of the attention work-order plan (0: the batch is too large to plan and
+// the items run in chunk-slowest order).
+size_t attn_plan_bytes(int B, int n_kv, int max_chunks);
 int attention_launch(const AttnArgs &a, int rows_max, const int32_t *packed_req, int waves,
                      hipStream_t s);
 

@@ -24,7 +24,7 @@ static int attn_chunk(const dcut_layer_cfg *c, int B) {
 }
 
 struct LayerWs {
-  size_t h, q, attn, rope, part, mid, split, moe, total;
+  size_t h, q, attn, rope, part, plan, mid, split, moe, total;
   int split_qkv, split_o, split_down;
 };
 
@@ -59,6 +59,7 @@ static LayerWs layer_ws(const dcut_layer_cfg *c, int B, int D) {
   w.attn = off; off = align256(off + M * qd * 2);
   w.rope = off; off = align256(off + M * (c->head_dim / 2) * sizeof(float2));
   w.part = off; off = align256(off + M * c->n_q * (size_t)mc * (c->head_dim + 2) * sizeof(float));
+  w.plan = off; off = align256(off + attn_plan_bytes(B, c->n_kv, mc));
   w.mid = off; off = align256(off + (c->n_exp == 0 ? M * (size_t)c->inter * 2 : 0));
   const size_t nqkv = (size_t)(c->n_q + 2 * c->n_kv) * c->head_dim;
   w.split_qkv = gemm_splits((int)M, (int)nqkv, c->hidden);
@@ -135,6 +136,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   at.cu = cu; at.ctx_len = ctx_len; at.B = B; at.D = D; at.n_q = nq; at.n_kv = nkv; at.head_dim = hd;
   at.chunk = attn_chunk(cfg, B); at.max_chunks = (cfg->max_ctx + at.chunk - 1) / at.chunk;
   at.part = part; at.out = att; at.dev_err = dev_err;
+  at.plan = attn_plan_bytes(B, nkv, at.max_chunks) ? (int32_t *)(base + L.plan) : nullptr;
   const int waves = ((nq / nkv) * (D + 1) + 15) / 16;
   DCUT_TRY(attention_launch(at, M, packed_req, waves, stream));
   // 4. O projection + residual

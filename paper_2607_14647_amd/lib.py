@@ -20,7 +20,7 @@ OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
 DERR_CONF, DERR_TOKEN, DERR_CAPACITY = 1, 2, 4
 KERNELS = dict(NONE=0, SELECT=1, PACK=2, NORM=3, GEMM_QKV=4, ATTN=5, ATTN_COMBINE=6, GEMM_O=7,
                GEMM_GATE_UP=8, GEMM_DOWN=9, MOE=10, LM_HEAD=11, ARGMAX_FINAL=12, ACCEPT=13,
-               RS_DECIDE=14, RS_RESIDUAL=15, RS_FINISH=16)
+               RS_DECIDE=14, RS_RESIDUAL=15, RS_FINISH=16, ATTN_PLAN=17)
 RS_SCAN, RS_FIXED, RS_HISTORY = 0, 1, 2
 
 EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",

@@ -44,6 +44,9 @@ def tiny_variants():
                                       layer=dataclasses.replace(c1.layer, n_q=8, n_kv=1, inter=0,
                                                                 n_exp=128, top_k=8, exp_inter=64,
                                                                 rope_theta=1e6)),
+        # more than 512 attention work items (72 requests x 2 kv heads x 4 chunks of 512 keys),
+        # so they run in the longest-first planned order; contexts down to zero
+        "plan": dataclasses.replace(c1, cid=88, B=72, ctx=("uniform", 0, 2000), budgets=(200,)),
         # head_dim 128, split-K QKV (RoPE in the reduce pass), O and down projections, and a
         # vocabulary wide enough for the 256 x 256 LM-head tiles
         "split": dataclasses.replace(c1, cid=87, budgets=(40,),

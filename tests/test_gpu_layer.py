@@ -95,6 +95,26 @@ def test_layer_parity(name, seed):
     assert np.array_equal(ml, logits[np.arange(K), am])
 
 
+def test_attention_plan_runs_every_item():
+    """The layer scratch is filled with NaN bit patterns before the call, so an attention
+    work item that the longest-first plan dropped would leave NaN partials or rows."""
+    need_gpu()
+    cfg = VARIANTS["plan"]
+    st, w, kv = workload(cfg, 0)
+    K = cfg.budgets[0]
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    vs.ws_layer.fill_(255)
+    vs.select([K], [1.0])
+    vs.verify()
+    torch.cuda.synchronize()
+    sel, lay, _, _ = _oracle(cfg, st, olay.prepare_weights(w), kv, K)
+    x = vs.x.cpu().numpy()[:K]
+    assert np.isfinite(x).all()
+    ex = row_rel_err(x, lay["x_out"])
+    note(f"plan variant: B={cfg.B}, {K} rows, x err {ex.max():.2e}")
+    assert ex.max() <= X_RTOL
+
+
 @pytest.mark.parametrize("name", ["cfg1", "long"])
 def test_end_to_end_accept_with_forced_drafts(name):
     """Drafts forced from the oracle's greedy tokens; acceptance must match the oracle."""
