@@ -55,6 +55,19 @@ def tiny_variants():
     }
 
 
+def edge_variants():
+    """The tiny layer at the size limits of the layer call."""
+    c1 = wl.CONFIGS[1]
+    return {
+        # the largest batch and row count: B = 4096, B(D+1) = 8192; attention work items in
+        # chunk-slowest order (batches above 1024 are not planned)
+        "maxb": dataclasses.replace(c1, cid=89, B=4096, D=1, ctx=("uniform", 0, 64), budgets=(6000,)),
+        # the largest planned batch: one request per thread of the planning workgroup, with full
+        # and ragged chunks of 1024 keys
+        "plan1024": dataclasses.replace(c1, cid=90, B=1024, D=3, ctx=("uniform", 0, 2500), budgets=(2500,)),
+    }
+
+
 @functools.lru_cache(maxsize=8)
 def workload(cfg: wl.Config, seed: int, with_kv: bool = True):
     st = wl.make_step_inputs(cfg, seed)

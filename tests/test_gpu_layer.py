@@ -16,11 +16,12 @@ from oracle import lm_head as olm
 from oracle import select as osel
 from paper_2607_14647_amd import lib as L
 from paper_2607_14647_amd import runner
-from tests.gpu_common import (ARGMAX_GAP, LOGIT_RTOL, ROUTER_GAP, X_RTOL, need_gpu, note,
+from tests.gpu_common import (ARGMAX_GAP, LOGIT_RTOL, ROUTER_GAP, X_RTOL, edge_variants, need_gpu, note,
                               row_rel_err, tiny_variants, workload)
 
 pytestmark = pytest.mark.gpu
 VARIANTS = tiny_variants()
+EDGES = edge_variants()
 
 
 def _gpu_run(cfg, st, w, kv, budgets, costs, draft=None):
@@ -50,7 +51,16 @@ def _oracle(cfg, st, w64, kv, K, draft=None):
 @pytest.mark.parametrize("seed", [0, 1])
 def test_layer_parity(name, seed):
     need_gpu()
-    cfg = VARIANTS[name]
+    _layer_parity(VARIANTS[name], name, seed)
+
+
+@pytest.mark.parametrize("name", list(EDGES))
+def test_layer_parity_at_the_limits(name):
+    need_gpu()
+    _layer_parity(EDGES[name], name, 0)
+
+
+def _layer_parity(cfg, name, seed):
     st, w, kv = workload(cfg, seed)
     w64 = olay.prepare_weights(w)
     K = cfg.budgets[0]
@@ -95,11 +105,12 @@ def test_layer_parity(name, seed):
     assert np.array_equal(ml, logits[np.arange(K), am])
 
 
-def test_attention_plan_runs_every_item():
+@pytest.mark.parametrize("name", ["plan", "plan1024"])
+def test_attention_plan_runs_every_item(name):
     """The layer scratch is filled with NaN bit patterns before the call, so an attention
     work item that the longest-first plan dropped would leave NaN partials or rows."""
     need_gpu()
-    cfg = VARIANTS["plan"]
+    cfg = {**VARIANTS, **EDGES}[name]
     st, w, kv = workload(cfg, 0)
     K = cfg.budgets[0]
     vs = runner.VerifyStep(cfg, w, st, kv)
@@ -111,7 +122,7 @@ def test_attention_plan_runs_every_item():
     x = vs.x.cpu().numpy()[:K]
     assert np.isfinite(x).all()
     ex = row_rel_err(x, lay["x_out"])
-    note(f"plan variant: B={cfg.B}, {K} rows, x err {ex.max():.2e}")
+    note(f"plan variant {name}: B={cfg.B}, {K} rows, x err {ex.max():.2e}")
     assert ex.max() <= X_RTOL
 
 
