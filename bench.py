@@ -76,6 +76,43 @@ def roofline(name, cfg, K, ctx_len, us):
                 frac=round(ach / PEAK_HBM_GBS, 4), flops=fl, bytes=by)
 
 
+def kernel_fraction(name, cfg, K, ctx_len, us):
+    """Fraction of the roofline time max(bytes / HBM peak, flops / bf16 peak) that a
+    kernel with algorithmic work reaches; None for latency-bound kernels."""
+    fl, by = kernel_work(name, cfg, K, ctx_len)
+    if by <= 0 or us <= 0:
+        return None
+    ideal_us = max(by / (PEAK_HBM_GBS * 1e9), fl / (PEAK_BF16_TFLOPS * 1e12)) * 1e6
+    return dict(bound="mfma" if fl / by > RIDGE else "hbm", ideal_us=round(ideal_us, 2), us=us,
+                frac=round(ideal_us / us, 4))
+
+
+# launches per step of each kernel that the counter summary covers (per decoder layer
+# where the kernel belongs to the layer); O and down share one kernel and one entry
+COUNTED_LAUNCHES = {"LM_HEAD": (1, False), "GEMM_GATE_UP": (1, True), "GEMM_QKV": (1, True),
+                    "ATTN": (1, True), "GEMM_O+DOWN": (2, True)}
+
+
+def counted_step_bytes(workload, K, layers):
+    """HBM bytes per step of the kernels in the committed counter summary, when it
+    was taken on the current sources, the same workload and K*; else None."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        t = json.load(open(p))
+    except ValueError:
+        return None
+    total, kernels = 0.0, []
+    for kid, (n, per_layer) in COUNTED_LAUNCHES.items():
+        e = t.get(kid)
+        if not e or e.get("source_hash") != source_hash() or e.get("workload") != workload or e.get("K") != K:
+            return None
+        total += e["bytes_per_launch"] * n * (layers if per_layer else 1)
+        kernels.append(kid)
+    return total, kernels
+
+
 def source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_14647_amd", "csrc")
@@ -112,6 +149,21 @@ def cpu_baseline(cfg, st, w, kv, budgets, costs, target_s=15.0):
 
     info = threadpoolctl.threadpool_info()
     cores = max([d.get("num_threads", 1) for d in info] + [1])
+    cpu_model = "unknown"
+    try:
+        cpu_model = next((l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name")),
+                         "unknown")
+    except OSError:
+        pass
+    blas = sorted({d.get("internal_api", "?") for d in info if d.get("user_api") == "blas"})
+    # the selection alone, single-threaded, median of 3
+    with threadpoolctl.threadpool_limits(1):
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            osel.select(st["conf"], st["draft"], st["ctx_len"], budgets, costs)
+            ts.append(time.perf_counter() - t0)
+    select_ms = 1000.0 * statistics.median(ts)
     log(f"cpu baseline: converting weights (BLAS threads {cores})")
     w64 = olay.prepare_weights(w)
     ly = cfg.layer
@@ -149,7 +201,9 @@ def cpu_baseline(cfg, st, w, kv, budgets, costs, target_s=15.0):
     return dict(value=round(tokens * passes / dt, 2), unit="accepted tokens/s", cores=int(cores), kind="oracle",
                 sample=f"requests 0..{n - 1} of the batch ({nrows} kept rows, {tokens} accepted tokens): "
                        f"full-batch selection, then the float64 layer + LM head + accept for the sample; "
-                       f"{passes} passes, {dt:.1f} s", seconds=round(dt, 2))
+                       f"{passes} passes, {dt:.1f} s", seconds=round(dt, 2),
+                select_ms_1thread=round(select_ms, 2), cpu_model=cpu_model, cpu_count=os.cpu_count(),
+                affinity=len(os.sched_getaffinity(0)), blas=blas)
 
 
 def main():
@@ -319,6 +373,28 @@ def main():
     stop.record(stream)
     torch.cuda.synchronize()
     L.profile_arm("NONE")
+    # per-step distribution (events around each step, outside the timed region); a
+    # profiler replay of saved state runs the timed steps only
+    step_dist, cold = None, None
+    if state is None:
+        per_step = sorted(timed(adaptive, 100))
+        step_dist = dict(median_ms=round(statistics.median(per_step), 4),
+                         p95_ms=round(per_step[int(0.95 * len(per_step)) - 1], 4), reps=len(per_step))
+    if flush is None and state is None:
+        # cold cache: a 512 MB write before each step evicts the 256 MB MALL (not timed)
+        fl = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+        for a, b in evs:
+            fl.fill_(1)
+            a.record(stream)
+            adaptive()
+            b.record(stream)
+        torch.cuda.synchronize()
+        cms = statistics.median(a.elapsed_time(b) for a, b in evs)
+        cold = dict(median_ms=round(cms, 4), tokens_per_s=round(int(vs.total.item()) / (cms * 1e-3), 1), reps=20)
+        del fl
+        log(f"per step: median {step_dist['median_ms']} ms, p95 {step_dist['p95_ms']} ms; "
+            f"cold median {cms:.4f} ms")
     graph = None
     if args.graph:
         g = vs.capture(adaptive)
@@ -389,6 +465,9 @@ def main():
     rl["traffic"] = measured_traffic(dominant, workload, Kstar)
     rl["kernel"] = dominant
     rl["avg_us"] = round(dom_us, 2)
+    fractions = {k: kernel_fraction(k, cfg, Kstar, st["ctx_len"], v) for k, v in breakdown.items()}
+    fractions = {k: v for k, v in fractions.items() if v is not None}
+    counted = counted_step_bytes(workload, Kstar, args.layers) if args.temperature == 0 else None
     fixed = {}
     for rho, m in (("0.25", 4), ("0.50", 8), ("0.75", 12), ("1.00", 16)):
         K = cfg.B * m
@@ -416,8 +495,13 @@ def main():
                      f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})")),
         hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         step_algorithmic_bytes=int(step_bytes),
+        hbm_counted=None if counted is None else dict(
+            gbps=round(counted[0] / (ms_per_step * 1e-3) / 1e9, 1), bytes=int(counted[0]), kernels=counted[1]),
         roofline=rl,
         kernel_us=breakdown,
+        kernel_roofline=fractions,
+        step_ms=step_dist,
+        cold=cold,
         cost_row_ms=[round(c, 4) for c in cost_ms],
         accepted_per_budget=acc_per_k,
         fixed_ratio=fixed,
