@@ -9,7 +9,7 @@
 // [L_i, L_i + d_i).  The chunking depends on L_i only, never on d_i, so a row's
 // partial results are the same whichever later rows are kept.  All G = n_q/n_kv
 // query heads of the group and all d_i kept rows (G*d_i <= 256 rows, 16 per
-// wave) share each 64-key tile, so the cache is read from HBM exactly once.
+// wave) share each 32-key tile, so the cache is read from HBM exactly once.
 //
 // Per tile and wave (v_mfma_f32_16x16x32_bf16):
 //   S^T[key][row] = K[key][:] . Q[row][:]   -> lane (row = lane%16) owns keys
@@ -53,8 +53,9 @@ __device__ __forceinline__ int n_chunks(int L, int chunk, int MC) {
 // kv head fastest within a request's last chunk.  Requests with no kept rows
 // have no items.  One workgroup (k_attn_plan, one thread per request) ranks
 // the requests and writes the item list and its length; attention workgroup b
-// takes item b, and those past the end exit at once.  The results do not depend on the order: every
-// item writes its own partial, merged in chunk order.
+// takes item b, and those past the end exit at once.  The results do not
+// depend on the order: every item writes its own partial, merged in chunk
+// order.
 //
 // Plan layout: int32 count at offset 0, items from byte 256 on, 8 int32 each:
 // {request, kv head, chunk, first packed row, kept rows, usable context, cap, 0}.
