@@ -326,8 +326,8 @@ def main():
     adaptive = lambda: run_step(budgets, cost_ms)
 
     # 4. per-kernel breakdown with the timing hook
-    names = ["SELECT", "NORM", "GEMM_QKV"] + (["ATTN_PLAN"] if cfg.B <= 1024 else []) + [
-        "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "LM_HEAD", "ARGMAX_FINAL"]
+    names = ["SELECT", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN",
+             "LM_HEAD", "ARGMAX_FINAL"]
     names += ["RS_DECIDE", "RS_RESIDUAL", "RS_FINISH"] if args.rs else ["ACCEPT"]
     breakdown = {} if state is None else state["kernel_us"]
     for nm in (names if state is None else []):
@@ -343,7 +343,7 @@ def main():
         torch.cuda.synchronize()
         breakdown[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
     # the dominant kernel by time per step: layer kernels launch once per decoder layer
-    per_layer = {"GEMM_QKV", "ATTN_PLAN", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "MOE"}
+    per_layer = {"GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "MOE"}
     dominant = max(breakdown, key=lambda k: breakdown[k] * (args.layers if k in per_layer else 1))
     if args.state and state is None:
         json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,

@@ -356,7 +356,9 @@ enum {
   DCUT_KERNEL_GEMM_QKV, DCUT_KERNEL_ATTN, DCUT_KERNEL_ATTN_COMBINE, DCUT_KERNEL_GEMM_O,
   DCUT_KERNEL_GEMM_GATE_UP, DCUT_KERNEL_GEMM_DOWN, DCUT_KERNEL_MOE, DCUT_KERNEL_LM_HEAD,
   DCUT_KERNEL_ARGMAX_FINAL, DCUT_KERNEL_ACCEPT, DCUT_KERNEL_RS_DECIDE, DCUT_KERNEL_RS_RESIDUAL,
-  DCUT_KERNEL_RS_FINISH, DCUT_KERNEL_ATTN_PLAN /* attention work order, batches up to 1024 */
+  DCUT_KERNEL_RS_FINISH,
+  DCUT_KERNEL_ATTN_PLAN /* no kernel of its own: the attention work order is built by an extra
+                           workgroup of the layer's first norm kernel */
 };
 int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop);
 

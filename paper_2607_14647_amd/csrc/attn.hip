@@ -20,6 +20,12 @@
 //                   V^T operand), V staged transposed in LDS.
 // Partial (o, m, l) per (row, head, chunk) are merged in chunk order by
 // k_attn_combine; a request with a single chunk is finished in place.
+//
+// Workgroup b takes item b of the longest-first work order (attn_plan.h),
+// which the layer's first norm kernel builds in one extra workgroup; batches
+// too large to plan and grids of one round of slots number the items
+// arithmetically, chunk index slowest.
+#include "attn_plan.h"
 #include "dcut_internal.h"
 
 namespace dcut {
@@ -28,131 +34,6 @@ namespace {
 
 constexpr int KT = 32;     // keys per tile
 constexpr int NSTAGE = 4;  // LDS ring stages: three tiles in flight while one is used
-
-// Cached length used for request i (clamped so bad device data stays in bounds)
-// and its number of chunks (at least one: the block keys).
-__device__ __forceinline__ int usable_ctx(int L, int cap, int D) {
-  int hi = cap - D - 1;
-  if (L > hi) L = hi;
-  return L < 0 ? 0 : L;
-}
-__device__ __forceinline__ int n_chunks(int L, int chunk, int MC) {
-  int nc = L > 0 ? (L + chunk - 1) / chunk : 1;
-  return nc > MC ? MC : nc;
-}
-
-// Work order.  Workgroups are dispatched in blockIdx order as slots free up,
-// so ordering the live items by work length, longest first, makes the
-// hardware dispatcher run a longest-processing-time-first schedule: the short
-// ragged last chunks fill the gaps at the end instead of a long item starting
-// last.  An item's work is its key count: a full chunk has CH keys, a
-// request's last chunk L - (nc-1)*CH + d.  The order is
-//   1. last chunks longer than CH, by length descending (ties: request index),
-//   2. all full chunks, request by request, chunk then kv head,
-//   3. the remaining last chunks, by length descending (ties: request index),
-// kv head fastest within a request's last chunk.  Requests with no kept rows
-// have no items.  One workgroup (k_attn_plan, one thread per request) ranks
-// the requests and writes the item list and its length; attention workgroup b
-// takes item b, and those past the end exit at once.  The results do not
-// depend on the order: every item writes its own partial, merged in chunk
-// order.
-//
-// Plan layout: int32 count at offset 0, items from byte 256 on, 8 int32 each:
-// {request, kv head, chunk, first packed row, kept rows, usable context, cap, 0}.
-constexpr int PLAN_MAX_B = 1024;
-constexpr int PLAN_HEAD = 256;
-constexpr int PLAN_MIN_ITEMS = 512;   // two 512-thread workgroups per compute unit
-
-__global__ void __launch_bounds__(1024) k_attn_plan(AttnArgs a) {
-  // per request: sort key, inverse rank, first full-chunk item, row range,
-  // usable context, cap, last chunk index
-  __shared__ __align__(16) int s_ck[PLAN_MAX_B];
-  __shared__ int s_inv[PLAN_MAX_B], s_pre[PLAN_MAX_B], s_t0[PLAN_MAX_B], s_d[PLAN_MAX_B];
-  __shared__ int s_L[PLAN_MAX_B], s_cap[PLAN_MAX_B], s_last[PLAN_MAX_B];
-  __shared__ int s_w[3 * 16];
-  const int B = a.B, CH = a.chunk, MC = a.max_chunks, nkv = a.n_kv;
-  const int B4 = (B + 3) & ~3;
-  const int j = threadIdx.x, w = j >> 6, ln = j & 63;
-  int key = -1, full = 0;
-  if (j < B) {
-    const int t0 = a.cu[j];
-    const int d = a.cu[j + 1] - t0;
-    const int L0 = a.ctx_len[j];
-    const int cap = a.kv_cap[j];
-    if (d > 0 && (L0 < 0 || L0 + a.D + 1 > cap) && a.dev_err) atomicOr(a.dev_err, DCUT_DERR_CAPACITY);
-    const int L = usable_ctx(L0, cap, a.D);
-    const int nc = n_chunks(L, CH, MC);
-    if (d > 0) {
-      key = min(L + d - (nc - 1) * CH, 1 << 20);   // only a cap beyond max_ctx makes it larger
-      full = nc - 1;
-    }
-    s_t0[j] = t0; s_d[j] = d; s_L[j] = L; s_cap[j] = cap; s_last[j] = nc - 1;
-  }
-  // sort key: length descending, then request index ascending (key <= 2^20,
-  // B <= 1024), so a request's rank is the number of larger keys
-  const int ck = key > 0 ? (key << 10) | (1023 - j) : -1;
-  if (j < B4) s_ck[j] = ck;
-  int x = full;                                   // inclusive scan within the wave
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (ln >= o) x += y;
-  }
-  const unsigned long long bl = __ballot(key > CH), bv = __ballot(key > 0);
-  if (ln == 63) s_w[w] = x;
-  if (ln == 0) {
-    s_w[16 + w] = __popcll(bl);
-    s_w[32 + w] = __popcll(bv);
-  }
-  __syncthreads();
-  int before = 0, n_full = 0, n_long = 0, n_live = 0;
-  for (int v = 0; v < 16; ++v) {
-    const int sv = s_w[v];
-    before += v < w ? sv : 0;
-    n_full += sv;
-    n_long += s_w[16 + v];
-    n_live += s_w[32 + v];
-  }
-  if (ck >= 0) {
-    int rank = 0;
-    const int4 *k4 = (const int4 *)s_ck;
-#pragma unroll 4
-    for (int k = 0; k < (B4 >> 2); ++k) {
-      const int4 v = k4[k];
-      rank += (v.x > ck) + (v.y > ck) + (v.z > ck) + (v.w > ck);
-    }
-    s_inv[rank] = j;
-  }
-  if (j < B) s_pre[j] = (before + x - full) * nkv;
-  __syncthreads();
-  // consecutive threads write consecutive items
-  const int e1 = n_long * nkv, e2 = e1 + n_full * nkv, e3 = e2 + (n_live - n_long) * nkv;
-  int32_t *plan = a.plan;
-  if (j == 0) plan[0] = e3;
-  int4 *items = (int4 *)((char *)plan + PLAN_HEAD);
-  for (int p = j; p < e3; p += 1024) {
-    int i, g, c;
-    if (p < e1 || p >= e2) {
-      const int r = p < e1 ? p / nkv : n_long + (p - e2) / nkv;
-      i = s_inv[r];
-      g = (p < e1 ? p : p - e2) % nkv;
-      c = s_last[i];
-    } else {
-      // the last request whose first full-chunk item is at or before f
-      const int f = p - e1;
-      int lo = 0, hi = B;
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (s_pre[mid] <= f) lo = mid; else hi = mid;
-      }
-      i = lo;
-      c = (f - s_pre[i]) / nkv;
-      g = (f - s_pre[i]) % nkv;
-    }
-    items[2 * p] = make_int4(i, g, c, s_t0[i]);
-    items[2 * p + 1] = make_int4(s_d[i], s_L[i], s_cap[i], 0);
-  }
-}
 
 typedef short short4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -500,7 +381,6 @@ int launch_hd(const AttnArgs &a, int rows_max, const int32_t *packed_req, int wa
   // at least 8 waves: the extra waves share the tile loads, which measured
   // faster than 4 waves per workgroup (16 waves measured slower)
   const dim3 grid(a.B * a.n_kv * a.max_chunks);
-  if (a.plan) DCUT_TRY(launch(DCUT_KERNEL_ATTN_PLAN, k_attn_plan, dim3(1), dim3(1024), 0, s, a));
   if (waves <= 8) {
     DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 8>, grid, dim3(512), 0, s, a));
   } else {

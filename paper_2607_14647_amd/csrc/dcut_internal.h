@@ -161,10 +161,15 @@ int gemm_splits(int M_max, int N, int K);
 // norm that reads its result.  One workgroup per live row; H % 8 == 0, H <= 8192.
 int reduce_rmsnorm_launch(int kid, const float *part, int splits, int M_max, int H, const int32_t *m_count,
                           float *x, const uint16_t *gain, float eps, uint16_t *h_out, hipStream_t s);
+struct AttnArgs;
+// Row RMSNorm over the live rows (see norm.hip).  With `plan` (nullable; B <=
+// 1024 and plan->plan set) one extra workgroup also writes that attention
+// call's work order.
 int rmsnorm_launch(int kid, const float *x_in, const uint16_t *embed, const int32_t *tok, int vocab,
                    const uint16_t *gain, float eps, int H, int M_max, const int32_t *m_count,
                    float *x_copy, uint16_t *h_out, const int32_t *pos, int head_dim, float theta,
-                   float2 *rope_cs, unsigned long long *amax_init, int32_t *dev_err, hipStream_t s);
+                   float2 *rope_cs, unsigned long long *amax_init, int32_t *dev_err, const AttnArgs *plan,
+                   hipStream_t s);
 
 // Routed MoE MLP over the rows of h (bf16, [M_max][H]); adds into x_out.
 struct MoeArgs {

@@ -116,10 +116,18 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   const int M = B * (D + 1);
   const int32_t *Kstar = cu + B;
 
-  // 1. norm1 (+ embedding gather, residual copy, RoPE table)
+  // attention arguments (the work order is built by norm1)
+  AttnArgs at = {};
+  at.q = q; at.kv_k = kv->k; at.kv_v = kv->v; at.kv_base = kv->base; at.kv_cap = kv->cap;
+  at.cu = cu; at.ctx_len = ctx_len; at.B = B; at.D = D; at.n_q = nq; at.n_kv = nkv; at.head_dim = hd;
+  at.chunk = attn_chunk(cfg, B); at.max_chunks = (cfg->max_ctx + at.chunk - 1) / at.chunk;
+  at.part = part; at.out = att; at.dev_err = dev_err;
+  at.plan = attn_plan_bytes(B, nkv, at.max_chunks) ? (int32_t *)(base + L.plan) : nullptr;
+
+  // 1. norm1 (+ embedding gather, residual copy, RoPE table, attention work order)
   DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x_in, w->embed, packed_tok, cfg->vocab, w->attn_norm,
                           cfg->rms_eps, H, M, Kstar, x_out, h, packed_pos, hd, cfg->rope_theta,
-                          rope, nullptr, dev_err, stream));
+                          rope, nullptr, dev_err, &at, stream));
   // 2. QKV + RoPE + cache append
   GemmArgs g = {};
   g.A = h; g.lda = H; g.K = H; g.M_max = M; g.m_count = Kstar;
@@ -131,12 +139,6 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   g.splits = L.split_qkv; g.split_part = split;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_QKV, EPI_QKV_ROPE, g, stream));
   // 3. attention
-  AttnArgs at = {};
-  at.q = q; at.kv_k = kv->k; at.kv_v = kv->v; at.kv_base = kv->base; at.kv_cap = kv->cap;
-  at.cu = cu; at.ctx_len = ctx_len; at.B = B; at.D = D; at.n_q = nq; at.n_kv = nkv; at.head_dim = hd;
-  at.chunk = attn_chunk(cfg, B); at.max_chunks = (cfg->max_ctx + at.chunk - 1) / at.chunk;
-  at.part = part; at.out = att; at.dev_err = dev_err;
-  at.plan = attn_plan_bytes(B, nkv, at.max_chunks) ? (int32_t *)(base + L.plan) : nullptr;
   const int waves = ((nq / nkv) * (D + 1) + 15) / 16;
   DCUT_TRY(attention_launch(at, M, packed_req, waves, stream));
   // 4. O projection + residual
@@ -154,7 +156,8 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
                                    cfg->rms_eps, h, stream));
   else
     DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x_out, nullptr, nullptr, 0, w->mlp_norm, cfg->rms_eps, H,
-                            M, Kstar, nullptr, h, nullptr, 0, 0.0f, nullptr, nullptr, dev_err, stream));
+                            M, Kstar, nullptr, h, nullptr, 0, 0.0f, nullptr, nullptr, dev_err, nullptr,
+                            stream));
   // 6. MLP
   if (cfg->n_exp > 0) {
     MoeArgs me = {};

@@ -105,7 +105,7 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   float2 *part = (float2 *)((char *)keys + align256((size_t)M * slots * sizeof(unsigned long long)));
   const int32_t *Kstar = cu + B;
   DCUT_TRY(rmsnorm_launch(DCUT_KERNEL_NORM, x, nullptr, nullptr, 0, final_norm, eps, H, M, Kstar,
-                          nullptr, f, nullptr, 0, 0.0f, nullptr, nullptr, nullptr, stream));
+                          nullptr, f, nullptr, 0, 0.0f, nullptr, nullptr, nullptr, nullptr, stream));
   GemmArgs g = {};
   g.A = f; g.lda = H; g.K = H; g.M_max = M; g.m_count = Kstar;
   g.W = w_lm; g.ldw = H; g.N = V;

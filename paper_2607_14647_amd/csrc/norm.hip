@@ -5,6 +5,12 @@
 // norm of the layer), keeps a float32 copy of the residual, writes the
 // row's RoPE (cos, sin) table and clears the row's argmax key.  The sum of
 // squares is reduced in a fixed order, so the result is deterministic.
+//
+// The first norm of a layer also builds the attention work order in one extra
+// workgroup ahead of the rows (attn_plan.h): it needs only the batch layout,
+// which is known at the start of the layer, and running beside the rows it
+// costs no launch of its own.
+#include "attn_plan.h"
 #include "dcut_internal.h"
 
 namespace dcut {
@@ -17,9 +23,15 @@ k_rmsnorm(const float *__restrict__ x_in, const uint16_t *__restrict__ embed,
           int H, const int32_t *__restrict__ m_count, float *__restrict__ x_copy,
           uint16_t *__restrict__ h_out, const int32_t *__restrict__ pos, int head_dim, float theta,
           float2 *__restrict__ rope_cs, unsigned long long *__restrict__ amax_init,
-          int32_t *__restrict__ dev_err) {
+          int32_t *__restrict__ dev_err, AttnArgs plan) {
   __shared__ float s_red[4];
-  const int t = blockIdx.x;
+  extern __shared__ __align__(16) int plan_lds[];
+  // the plan workgroup is dispatched first: it takes longer than a row
+  if (plan.plan && blockIdx.x == 0) {
+    attn_plan_block<256>(plan, plan_lds);
+    return;
+  }
+  const int t = blockIdx.x - (plan.plan ? 1 : 0);
   if (t >= *m_count) return;
   const int tid = threadIdx.x;
 
@@ -167,9 +179,17 @@ int reduce_rmsnorm_launch(int kid, const float *part, int splits, int M_max, int
 int rmsnorm_launch(int kid, const float *x_in, const uint16_t *embed, const int32_t *tok, int vocab,
                    const uint16_t *gain, float eps, int H, int M_max, const int32_t *m_count,
                    float *x_copy, uint16_t *h_out, const int32_t *pos, int head_dim, float theta,
-                   float2 *rope_cs, unsigned long long *amax_init, int32_t *dev_err, hipStream_t s) {
-  return launch(kid, k_rmsnorm, dim3(M_max), dim3(256), 0, s, x_in, embed, tok, vocab, gain, eps, H,
-                m_count, x_copy, h_out, pos, head_dim, theta, rope_cs, amax_init, dev_err);
+                   float2 *rope_cs, unsigned long long *amax_init, int32_t *dev_err, const AttnArgs *plan,
+                   hipStream_t s) {
+  AttnArgs p = {};
+  size_t lds = 0;
+  if (plan && plan->plan) {
+    if (plan->B > PLAN_MAX_B) return DCUT_EINVAL;
+    p = *plan;
+    lds = attn_plan_lds_bytes(p.B, 256);
+  }
+  return launch(kid, k_rmsnorm, dim3(M_max + (p.plan ? 1 : 0)), dim3(256), lds, s, x_in, embed, tok, vocab, gain,
+                eps, H, m_count, x_copy, h_out, pos, head_dim, theta, rope_cs, amax_init, dev_err, p);
 }
 
 }  // namespace dcut
