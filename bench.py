@@ -49,6 +49,13 @@ def kernel_work(name, cfg, K, ctx_len):
     H, V, hd, nq, nkv = ly.hidden, ly.vocab, ly.head_dim, ly.n_q, ly.n_kv
     I = ly.inter
     nqkv = (nq + 2 * nkv) * hd
+    if ly.n_exp > 0 and name in ("GEMM_GATE_UP", "GEMM_DOWN"):
+        # grouped expert GEMMs over the K * top_k routed rows; every expert's weights are
+        # counted (with K * top_k >> n_exp nearly all of them are touched)
+        E, k, Ie = ly.n_exp, ly.top_k, ly.exp_inter
+        if name == "GEMM_GATE_UP":
+            return 2.0 * K * k * 2 * Ie * H, E * 2 * Ie * H * 2 + K * k * (H + Ie) * 2
+        return 2.0 * K * k * H * Ie, E * H * Ie * 2 + K * k * (Ie * 2 + H * 4)
     if name == "LM_HEAD":
         return 2.0 * K * V * H, V * H * 2 + K * H * 2 + K * 8
     if name == "GEMM_GATE_UP":

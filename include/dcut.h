@@ -349,7 +349,10 @@ int dcut_nearest_batch(int B, int n, const int32_t *captured);
 
 /* Kernel timing hook for profilers.  Arms `kernel` (a DCUT_KERNEL_* id) on the
  * calling thread: its next launches on this thread record `start` before and
- * `stop` after the kernel on the launch stream.  DCUT_KERNEL_NONE disarms. */
+ * `stop` after the kernel on the launch stream (an id launched several times
+ * per call keeps the last launch).  DCUT_KERNEL_NONE disarms.  In a routed-MoE
+ * layer the grouped expert GEMMs carry the GEMM_GATE_UP and GEMM_DOWN ids and
+ * the router, routing, grouping and combine kernels carry MOE. */
 enum {
   DCUT_KERNEL_NONE = 0, DCUT_KERNEL_SELECT /* selection and packing */,
   DCUT_KERNEL_PACK /* no kernel of its own: packing runs in the selection kernel */, DCUT_KERNEL_NORM,

@@ -683,10 +683,14 @@ int launch_epi(int kid, const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 int gemm_splits(int M_max, int N, int K) {
-  const int nMT = (M_max + Small::TM - 1) / Small::TM, nNT = (N + Small::TN - 1) / Small::TN;
+  // sized for at most 1024 rows: a large batch verifies far fewer than its
+  // B(D+1) rows at the budgets a cost row picks (a quarter of them is common),
+  // and splits sized for B(D+1) would leave most CUs idle there
+  const int M_ref = M_max < 1024 ? M_max : 1024;
+  const int nMT = (M_ref + Small::TM - 1) / Small::TM, nNT = (N + Small::TN - 1) / Small::TN;
   const int nk = (K + TK - 1) / TK;
   int sp = (1024 + nMT * nNT - 1) / (nMT * nNT);
-  const int cap = nk / 8 > 1 ? nk / 8 : 1;      // keep at least 8 k-slices per split
+  const int cap = nk / 16 > 1 ? nk / 16 : 1;    // keep at least 16 k-slices per split
   if (sp > cap) sp = cap;
   if (sp > 16) sp = 16;
   return sp < 1 ? 1 : sp;

@@ -232,13 +232,13 @@ int moe_launch(const MoeArgs &m, hipStream_t s) {
   gu.out_bf16 = mid; gu.ldo = m.inter;
   gu.tiles = tiles; gu.n_tiles = ntiles; gu.m_tiles = L.max_tiles; gu.w_stride = (long long)2 * m.inter * m.H;
   gu.a_rows = row_of; gu.a_extent = M;
-  DCUT_TRY(gemm_launch(DCUT_KERNEL_MOE, EPI_SWIGLU, gu, s));
+  DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_GATE_UP, EPI_SWIGLU, gu, s));
   GemmArgs dn = {};
   dn.A = mid; dn.lda = m.inter; dn.K = m.inter; dn.M_max = A; dn.m_count = m.m_count;
   dn.W = m.w_down; dn.ldw = m.inter; dn.N = m.H;
   dn.out_f32 = eo; dn.ldo = m.H;
   dn.tiles = tiles; dn.n_tiles = ntiles; dn.m_tiles = L.max_tiles; dn.w_stride = (long long)m.H * m.inter;
-  DCUT_TRY(gemm_launch(DCUT_KERNEL_MOE, EPI_STORE_F32, dn, s));
+  DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_DOWN, EPI_STORE_F32, dn, s));
   return launch(DCUT_KERNEL_MOE, k_moe_combine, dim3(M), dim3(256), 0, s, (const float *)eo,
                 (const int32_t *)inv, (const float *)wts, m.H, m.top_k, m.m_count, m.x_out);
 }

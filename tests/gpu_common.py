@@ -47,11 +47,15 @@ def tiny_variants():
         # more than 512 attention work items (72 requests x 2 kv heads x 4 chunks of 512 keys),
         # so they run in the longest-first planned order; contexts down to zero
         "plan": dataclasses.replace(c1, cid=88, B=72, ctx=("uniform", 0, 2000), budgets=(200,)),
-        # head_dim 128, split-K QKV (RoPE in the reduce pass), O and down projections, and a
-        # vocabulary wide enough for the 256 x 256 LM-head tiles
+        # head_dim 128, split-K O and down projections, and a vocabulary wide enough for the
+        # 256 x 256 LM-head tiles
         "split": dataclasses.replace(c1, cid=87, budgets=(40,),
-                                     layer=dataclasses.replace(c1.layer, hidden=1024, n_q=8, n_kv=2,
+                                     layer=dataclasses.replace(c1.layer, hidden=1024, n_q=16, n_kv=4,
                                                                head_dim=128, inter=2048, vocab=65536)),
+        # split-K QKV (RoPE and the cache append in the reduce pass) as well: K = 2048
+        "qkvsplit": dataclasses.replace(c1, cid=91, budgets=(40,),
+                                        layer=dataclasses.replace(c1.layer, hidden=2048, n_q=16, n_kv=4,
+                                                                  head_dim=128, inter=2048, vocab=1024)),
     }
 
 

@@ -42,7 +42,7 @@ def _candidates(cfg):
     return budgets, costs
 
 
-@pytest.mark.parametrize("name", ["cfg1", "split", "moe", "long", "plan"])
+@pytest.mark.parametrize("name", ["cfg1", "split", "qkvsplit", "moe", "long", "plan"])
 def test_graph_greedy_step(name):
     need_gpu()
     cfg = VARIANTS[name]

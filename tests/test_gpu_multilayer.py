@@ -36,7 +36,7 @@ def _kv_err(kg, vg, kv, lay, sel, ly, rows):
     return max(err)
 
 
-@pytest.mark.parametrize("name,n_layers", [("cfg1", 4), ("split", 3), ("moe", 3), ("long", 2)])
+@pytest.mark.parametrize("name,n_layers", [("cfg1", 4), ("split", 3), ("qkvsplit", 2), ("moe", 3), ("long", 2)])
 def test_layer_stack(name, n_layers):
     need_gpu()
     cfg = VARIANTS[name]
