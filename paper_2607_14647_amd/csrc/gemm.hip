@@ -552,8 +552,10 @@ k_gemm(GemmArgs a) {
 }
 
 // Dense GEMM whose tile shape follows the live row count M (read on the device):
-// 128 x 256 tiles when 256 x 256 tiles would leave a quarter or more of the
-// persistent workgroups without a task, else 256 x 256.  Every element is the
+// SwiGLU: 128 x 256 tiles when they take fewer rounds of the persistent grid
+// than 256 x 256 tiles would (counting a 128-row task as half a 256-row one),
+// else 256 x 256.  Argmax LM head: 128 x 256 tiles with four W slices when the
+// last 256-row tile would be at most half full.  Every element is the
 // same sequence of MFMA k-steps in both shapes, so the choice never changes a
 // result bit.
 template <int EPI>
@@ -563,8 +565,11 @@ k_gemm_dual(GemmArgs a) {
   static_assert(MidDeep::THREADS == Big::THREADS && MidDeep::LDS <= Big::LDS, "one launch shape for both tiles");
   const int M = *a.m_count;
   if constexpr (EPI == EPI_SWIGLU) {
-    const long long big_tasks = (long long)((M + Big::TM - 1) / Big::TM) * n_col_tiles<EPI>(a, Big::TN);
-    if (4 * big_tasks < 3LL * gridDim.x) gemm_tasks<EPI, Mid>(a);
+    // rounds of the persistent grid: a Mid task is half a Big one
+    const long long nct = n_col_tiles<EPI>(a, Big::TN), G = gridDim.x;
+    const long long big_rounds = ((M + Big::TM - 1) / Big::TM * nct + G - 1) / G;
+    const long long mid_rounds = ((M + Mid::TM - 1) / Mid::TM * nct + G - 1) / G;
+    if (mid_rounds < 2 * big_rounds) gemm_tasks<EPI, Mid>(a);
     else gemm_tasks<EPI, Big>(a);
   } else {
     if (lm_head_mid_tile(M)) gemm_tasks<EPI, MidDeep>(a);
