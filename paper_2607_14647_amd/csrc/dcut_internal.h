@@ -28,6 +28,40 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
   return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
 }
 
+// Split-K partial sums in split order, with the loads of four splits issued
+// together (one memory round trip per four splits).  load(s) returns split s;
+// indices past the last split re-read it, and the adds are selects rather than
+// branches, so the compiler keeps each batch of loads together.
+struct f4x2 {
+  float4 a, b;
+};
+__device__ __forceinline__ float2 add_if(bool use, float2 x, float2 y) {
+  return make_float2(use ? x.x + y.x : x.x, use ? x.y + y.y : x.y);
+}
+__device__ __forceinline__ float4 add_if(bool use, float4 x, float4 y) {
+  return make_float4(use ? x.x + y.x : x.x, use ? x.y + y.y : x.y, use ? x.z + y.z : x.z,
+                     use ? x.w + y.w : x.w);
+}
+__device__ __forceinline__ f4x2 add_if(bool use, f4x2 x, f4x2 y) {
+  return f4x2{add_if(use, x.a, y.a), add_if(use, x.b, y.b)};
+}
+template <typename T, typename Load>
+__device__ __forceinline__ T sum_splits(int splits, Load load) {
+  T v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) v[u] = load(u < splits ? u : splits - 1);
+  T acc = v[0];
+#pragma unroll
+  for (int u = 1; u < 4; ++u) acc = add_if(u < splits, acc, v[u]);
+  for (int s0 = 4; s0 < splits; s0 += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = load(s0 + u < splits ? s0 + u : splits - 1);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc = add_if(s0 + u < splits, acc, v[u]);
+  }
+  return acc;
+}
+
 // ---------------------------------------------------------------- profiling hook
 struct ProfileHook {
   int kernel;

@@ -585,14 +585,12 @@ k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
   if (m >= *m_count) return;
   const int n = (blockIdx.x * 256 + threadIdx.x) * 4;
   if (n >= N) return;
-  float4 acc = *(const float4 *)(part + (size_t)m * N + n);
-  for (int s = 1; s < splits; ++s) {
-    float4 v = *(const float4 *)(part + ((size_t)s * M_max + m) * N + n);
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-  }
   float4 *o = (float4 *)(out + (size_t)m * ldo + n);
+  const float4 x = accumulate ? *o : make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 acc = sum_splits<float4>(splits, [&](int s) {
+    return *(const float4 *)(part + ((size_t)s * M_max + m) * N + n);
+  });
   if (accumulate) {
-    float4 x = *o;
     acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
   }
   *o = acc;
@@ -609,14 +607,11 @@ k_qkv_reduce(GemmArgs a) {
   if (idx >= nh * half) return;
   const int head = idx / half, j = idx - head * half;
   const size_t c1 = (size_t)head * a.head_dim + j, c2 = c1 + half;
-  const float *p = a.split_part + (size_t)m * a.N;
-  float x1 = p[c1], x2 = p[c2];
-  for (int s = 1; s < a.splits; ++s) {
+  const float2 x = sum_splits<float2>(a.splits, [&](int s) {
     const float *q = a.split_part + ((size_t)s * a.M_max + m) * a.N;
-    x1 += q[c1];
-    x2 += q[c2];
-  }
-  qkv_emit(a, m, head, j, x1, x2);
+    return make_float2(q[c1], q[c2]);
+  });
+  qkv_emit(a, m, head, j, x.x, x.y);
 }
 
 int cu_count() {

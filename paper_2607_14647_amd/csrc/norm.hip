@@ -127,16 +127,13 @@ k_reduce_rmsnorm(const float *__restrict__ part, int splits, int M_max, int H,
   for (int q = 0; q < 4; ++q) {
     const int gi = tid + 256 * q;
     if (gi >= ng) break;
-    const float *p0 = part + (size_t)t * H + gi * 8;
-    float4 a = *(const float4 *)p0, b = *(const float4 *)(p0 + 4);
-    for (int sp = 1; sp < splits; ++sp) {
-      const float *ps = part + ((size_t)sp * M_max + t) * H + gi * 8;
-      const float4 c = *(const float4 *)ps, d = *(const float4 *)(ps + 4);
-      a.x += c.x; a.y += c.y; a.z += c.z; a.w += c.w;
-      b.x += d.x; b.y += d.y; b.z += d.z; b.w += d.w;
-    }
     float *xr = x + (size_t)t * H + gi * 8;
     const float4 xa = *(const float4 *)xr, xb = *(const float4 *)(xr + 4);
+    const f4x2 sum = sum_splits<f4x2>(splits, [&](int sp) {
+      const float *ps = part + ((size_t)sp * M_max + t) * H + gi * 8;
+      return f4x2{*(const float4 *)ps, *(const float4 *)(ps + 4)};
+    });
+    float4 a = sum.a, b = sum.b;
     a.x += xa.x; a.y += xa.y; a.z += xa.z; a.w += xa.w;
     b.x += xb.x; b.y += xb.y; b.z += xb.z; b.w += xb.w;
     *(float4 *)xr = a;
