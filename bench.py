@@ -384,9 +384,26 @@ def main():
     # profiler replay of saved state runs the timed steps only
     step_dist, cold = None, None
     if state is None:
-        per_step = sorted(timed(adaptive, 100))
-        step_dist = dict(median_ms=round(statistics.median(per_step), 4),
-                         p95_ms=round(per_step[int(0.95 * len(per_step)) - 1], 4), reps=len(per_step))
+        # each step bracketed by events, and its selection kernel timed by the hook (the
+        # paper reports the selector's p50/p95 too)
+        evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(100)]
+        for e in evs:
+            for x in e[2:]:
+                x.record(stream)
+        torch.cuda.synchronize()
+        for a, b, sa, sb in evs:
+            L.profile_arm("SELECT", sa, sb)
+            a.record(stream)
+            adaptive()
+            b.record(stream)
+        L.profile_arm("NONE")
+        torch.cuda.synchronize()
+        per_step = sorted(a.elapsed_time(b) for a, b, _, _ in evs)
+        sel_us = sorted(1000.0 * sa.elapsed_time(sb) for _, _, sa, sb in evs)
+        p95 = int(0.95 * len(per_step)) - 1
+        step_dist = dict(median_ms=round(statistics.median(per_step), 4), p95_ms=round(per_step[p95], 4),
+                         reps=len(per_step), select_median_us=round(statistics.median(sel_us), 2),
+                         select_p95_us=round(sel_us[p95], 2))
     if flush is None and state is None:
         # cold cache: a 512 MB write before each step evicts the 256 MB MALL (not timed)
         fl = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
