@@ -5,7 +5,8 @@ candidate budgets, device-side K*); selection is compared bit for bit over
 the whole batch, and the float64 oracle recomputes every kept row of a few
 sampled requests (the largest and smallest keep depth and the longest
 context).  Causality at full size: the sampled rows are bitwise identical
-under a second, smaller budget.
+under the smallest budget and under the quarter budget 4B (the budget the
+benchmark's cost row picks at batch 64).
 """
 import numpy as np
 import pytest
@@ -58,22 +59,24 @@ def test_fullsize_sampled_requests(cid):
     x_gpu = vs.x[torch.from_numpy(rows).cuda()].cpu().numpy()
     lg_gpu = logits[torch.from_numpy(rows).cuda()].cpu().numpy()
     am_gpu = vs.host("argmax")[rows]
-    # second run at the smallest budget for the causality check
-    vs.select([budgets[0]], [1.0])
-    vs.verify()
-    vs.lm_head(logits=logits)
-    torch.cuda.synchronize()
-    cu_p = vs.host("cu")
-    kl_p = vs.host("keep_len")
-    rows_p, rows_f = [], []
-    for i in sample:
-        for k in range(int(kl_p[i])):
-            rows_p.append(cu_p[i] + k)
-            rows_f.append(int(np.where(rows == sel["cu"][i] + k)[0][0]))
-    lg_p = logits[torch.tensor(rows_p, device="cuda")].cpu().numpy()
-    assert np.array_equal(lg_p, lg_gpu[rows_f]), "logits changed with the budget"
-    # the argmax too, whichever LM-head tile each live row count takes
-    assert np.array_equal(vs.host("argmax")[rows_p], am_gpu[rows_f]), "argmax changed with the budget"
+    # more runs at other budgets for the causality check
+    for Kc in sorted({budgets[0], 4 * cfg.B} & set(budgets)):
+        vs.select([Kc], [1.0])
+        vs.verify()
+        vs.lm_head(logits=logits)
+        torch.cuda.synchronize()
+        cu_p = vs.host("cu")
+        kl_p = vs.host("keep_len")
+        rows_p, rows_f = [], []
+        for i in sample:
+            for k in range(min(int(kl_p[i]), int(kl[i]))):
+                rows_p.append(cu_p[i] + k)
+                rows_f.append(int(np.where(rows == sel["cu"][i] + k)[0][0]))
+        note(f"cfg{cid}: causality at K={Kc}: {len(rows_p)} rows")
+        lg_p = logits[torch.tensor(rows_p, device="cuda")].cpu().numpy()
+        assert np.array_equal(lg_p, lg_gpu[rows_f]), f"logits changed with the budget (K={Kc})"
+        # the argmax too, whichever LM-head tile each live row count takes
+        assert np.array_equal(vs.host("argmax")[rows_p], am_gpu[rows_f]), f"argmax changed with the budget (K={Kc})"
     del logits
     note(f"cfg{cid}: oracle on requests {sample} ({len(rows)} rows)")
     w64 = olay.prepare_weights(w)
