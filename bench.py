@@ -220,7 +220,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cost-reps", type=int, default=10)
+    ap.add_argument("--cost-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold", action="store_true", help="evict the MALL between timed steps")
     ap.add_argument("--copy-bytes", type=int, default=0,
