@@ -147,7 +147,7 @@ __device__ __forceinline__ void qkv_emit(const GemmArgs &a, int gm, int head, in
 
 template <int EPI, class T>
 __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
-  constexpr int GM = T::GM, GN = T::GN, WM = T::WM, WN = T::WN, NWV = T::NWV;
+  constexpr int GN = T::GN, WM = T::WM, WN = T::WN, NWV = T::NWV;
   constexpr int TM = T::TM, TN = T::TN, NA = T::NA, NB = T::NB;
   constexpr int AJ = TM / (NWV * RPI), BJ = TN / (NWV * RPI);   // load instructions per wave per stage
   static_assert(AJ * NWV * RPI == TM && BJ * NWV * RPI == TN, "tile rows must fill whole wave loads");
