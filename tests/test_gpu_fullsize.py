@@ -91,3 +91,56 @@ def test_fullsize_sampled_requests(cid):
          f"rows compared {ok.sum()}/{len(rows)}")
     assert ex.max() <= X_RTOL and el.max() <= LOGIT_RTOL
     assert np.array_equal(am_gpu[sure], lm["argmax"][sure])
+
+
+def test_fullsize_sampled_lm_head():
+    """dcut_lm_head_sample at the batch-64 shape (V = 128256, 256 kept rows, the budget the
+    benchmark picks) with float32 logits and log-partition outputs, as the rejection-sampling step
+    launches it: sampled requests against the float64 oracle (logits within the logit tolerance,
+    the log-partition within that tolerance over T, the drawn token wherever the top-2 gap of the
+    noisy scores exceeds ARGMAX_GAP / T)."""
+    from oracle import rs as ors
+    from oracle import sampling as osm
+    from paper_2607_14647_amd import lib as L
+
+    need_gpu()
+    cfg = wl.CONFIGS[3]
+    ly = cfg.layer
+    st = wl.make_step_inputs(cfg, 0)
+    w = wl.make_weights(cfg, 0)
+    kv = wl.make_kv(cfg, 0, st["ctx_len"])
+    K, T, seed = 4 * cfg.B, 1.0, 0x5EED_0001
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    vs.select([K], [1.0])
+    vs.verify()
+    logits = torch.zeros(vs.rows, ly.vocab, dtype=torch.float32, device="cuda")
+    lse = torch.zeros(vs.rows, dtype=torch.float32, device="cuda")
+    L.lm_head_sample(ly.hidden, ly.vocab, cfg.B, cfg.D, vs.sel["cu"], vs.sel["packed_req"], vs.sel["packed_pos"],
+                     vs.x, vs.w["final_norm"], ly.rms_eps, vs.w["w_lm"], T, seed, vs.argmax, vs.ws_lm,
+                     max_score=vs.max_logit, logits=logits, lse=lse)
+    torch.cuda.synchronize()
+    assert int(vs.dev_err.item()) == 0
+    sel = osel.select(st["conf"], st["draft"], st["ctx_len"], [K], [1.0])
+    assert np.array_equal(vs.host("cu"), sel["cu"])
+    kl = sel["keep_len"]
+    sample = list(dict.fromkeys([int(np.argmax(kl)), int(np.argmin(kl)), int(np.argmax(st["ctx_len"]))]))
+    rows = np.concatenate([np.arange(sel["cu"][i], sel["cu"][i + 1]) for i in sample])
+    idx = torch.from_numpy(rows).cuda()
+    lg_gpu = logits[idx].cpu().numpy()
+    lse_gpu = lse[idx].cpu().numpy().astype(np.float64)
+    tok_gpu = vs.host("argmax")[rows]
+    del logits
+    note(f"cfg3 sampled LM head: oracle on requests {sample} ({len(rows)} rows)")
+    w64 = olay.prepare_weights(w)
+    lay = olay.verify_layer(ly, w64, kv, sel["cu"], sel["packed_tok"], sel["packed_pos"], sel["packed_req"],
+                            st["ctx_len"], cfg.D, requests=sample)
+    ref = osm.lm_head_sample(lay["x_out"][rows], w64["final_norm"], ly.rms_eps, w64["w_lm"],
+                             sel["packed_req"][rows], sel["packed_pos"][rows], T, seed)
+    el = row_rel_err(lg_gpu, ref["logits"])
+    scale = np.abs(ref["logits"]).max(axis=1)
+    e_lse = np.abs(lse_gpu - ors.lse_rows(ref["logits"], T)) / scale
+    sure = ref["gap"] > ARGMAX_GAP / T
+    note(f"  max rel err logits={el.max():.2e} lse={e_lse.max():.2e}; tokens checked {sure.sum()}/{len(rows)}")
+    assert el.max() <= LOGIT_RTOL and e_lse.max() <= LOGIT_RTOL / T
+    assert sure.sum() >= len(rows) // 2
+    assert np.array_equal(tok_gpu[sure], ref["token"][sure])
