@@ -93,3 +93,29 @@ def test_graph_rs_step(mode):
         g.replay()
         torch.cuda.synchronize()
         _same(_snapshot(vs), eager[rep])
+
+
+def test_graph_fullsize_step():
+    """The batch-64 step (dense 8B-shaped layer, V = 128256, all candidate budgets) captured
+    once and replayed after eager steps at another budget: every replay reproduces the eager
+    step bit for bit, including the attention work order built inside the graph."""
+    need_gpu()
+    cfg = wl.CONFIGS[3]
+    st = wl.make_step_inputs(cfg, 0)
+    w = wl.make_weights(cfg, 0)
+    kv = wl.make_kv(cfg, 0, st["ctx_len"])
+    vs = runner.VerifyStep(cfg, w, st, kv)
+    budgets = list(cfg.budgets)
+    costs = [1.0 + K / (2.0 * cfg.B) for K in budgets]
+    step = lambda: vs.step(budgets, costs)
+    step()
+    torch.cuda.synchronize()
+    ref = _snapshot(vs)
+    note(f"graph cfg3: K*={ref['choice'][0]}")
+    g = vs.capture(step)
+    for rep in range(3):
+        vs.step([budgets[-1]], [1.0])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _same(_snapshot(vs), ref)
