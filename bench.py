@@ -186,40 +186,48 @@ def cpu_baseline(cfg, st, w, kv, budgets, costs, target_s=15.0):
         g[rows] = lm["argmax"]
         acc = oacc.accept(z, sel["keep_len"], sel["cu"], g)
         dt = time.perf_counter() - t0
-        return dt, int(sum(int(acc["accept_len"][i]) + 1 for i in sample)), len(rows)
+        # requests whose deciding rows hold a near-tie of the top-2 logits (argmax gate 1e-2)
+        gap = np.full(len(g), np.inf)
+        gap[rows] = lm["gap"]
+        tie = [i for i in sample if (gap[sel["cu"][i]: sel["cu"][i] + acc["accept_len"][i] + 1] <= 1e-2).any()]
+        clear = int(sum(int(acc["accept_len"][i]) + 1 for i in sample if i not in tie))
+        return dt, int(sum(int(acc["accept_len"][i]) + 1 for i in sample)), len(rows), clear, tie
 
     # drafts of the sampled requests forced by the oracle itself (not timed)
     probe = [0]
     z = odr.force_matches(ly, w64, kv, st["conf"], st["draft"], st["match_u"], st["ctx_len"], cfg.D,
                           requests=probe)
-    dt1, _, _ = run(probe, z)
+    dt1 = run(probe, z)[0]
     n = int(max(1, min(cfg.B, target_s / max(dt1, 1e-3))))
     sample = list(range(n))
     log(f"cpu baseline: one request {dt1:.2f}s -> sample of {n} requests; forcing their drafts")
     z = odr.force_matches(ly, w64, kv, st["conf"], st["draft"], st["match_u"], st["ctx_len"], cfg.D,
                           requests=sample)
     # the same pass repeated until about 10 s of CPU work have run (the whole batch may take less)
-    dt, tokens, nrows = run(sample, z)
+    dt, tokens, nrows, clear, tie = run(sample, z)
     passes = 1
     while dt < 10.0:
-        d2, _, _ = run(sample, z)
-        dt += d2
+        dt += run(sample, z)[0]
         passes += 1
     return dict(value=round(tokens * passes / dt, 2), unit="accepted tokens/s", cores=int(cores), kind="oracle",
                 sample=f"requests 0..{n - 1} of the batch ({nrows} kept rows, {tokens} accepted tokens): "
                        f"full-batch selection, then the float64 layer + LM head + accept for the sample; "
                        f"{passes} passes, {dt:.1f} s", seconds=round(dt, 2),
                 select_ms_1thread=round(select_ms, 2), cpu_model=cpu_model, cpu_count=os.cpu_count(),
-                affinity=len(os.sched_getaffinity(0)), blas=blas)
+                affinity=len(os.sched_getaffinity(0)), blas=blas,
+                oracle_accepted=tokens, oracle_accepted_clear=clear, near_tie_requests=tie,
+                sample_requests=sample, draft_rows=[z[i].tolist() for i in sample])
 
 
-def main():
+def parse_args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--seed", type=int, default=None,
+                    help="one seed only (default: the greedy headline runs seeds 0-4 and reports their median; "
+                         "the other modes run seed 0)")
     ap.add_argument("--cost-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cold", action="store_true", help="evict the MALL between timed steps")
@@ -247,11 +255,18 @@ def main():
     ap.add_argument("--cost-table", action="store_true",
                     help="run the startup cost-table protocol over captured batch sizes 1, 8, 16, 32, 64 and "
                          "the ratio buckets 25/50/75/100 %% (each entry a graph-captured step, median of 10)")
+    ap.add_argument("--force-k", type=int, default=0,
+                    help="time the step at this one budget instead of the cost model's choice (no cost row, "
+                         "no CPU baseline); B(D+1) gives the unpruned step")
     ap.add_argument("--state", default=None,
                     help="JSON file with the forced drafts, cost row and dominant kernel of an earlier "
                          "run of the same workload; written when missing, reused when present (a "
                          "profiler run then sees only the timed adaptive steps at K*)")
-    args = ap.parse_args()
+    return ap.parse_args()
+
+
+def main():
+    args = parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: measures one GPU only; the verify step has no multi-GPU path. "
@@ -267,44 +282,17 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs an MI355X GPU"
     if args.rs and args.temperature == 0:
         args.temperature = 1.0
+    greedy_headline = not (args.rs or args.temperature > 0 or args.layers > 1 or args.state or args.force_k)
+    if args.seed is not None:
+        seeds = [args.seed]
+    else:
+        seeds = [0, 1, 2, 3, 4] if greedy_headline else [0]
     cfg = wl.CONFIGS[args.config]
     ly = cfg.layer
-    log(f"workload cfg{cfg.cid} ({cfg.name}) seed {args.seed}: generating")
-    t0 = time.time()
-    st = wl.make_step_inputs(cfg, args.seed)
-    w = wl.make_weights(cfg, args.seed)
-    kv = wl.make_kv(cfg, args.seed, st["ctx_len"])
-    log(f"generated in {time.time() - t0:.1f}s; uploading")
-    vs = runner.VerifyStep(cfg, w, st, kv)
-    for l in range(1, args.layers):
-        vs.add_layer(wl.make_weights(cfg, args.seed, layer=l), wl.make_kv(cfg, args.seed, st["ctx_len"], layer=l))
-        if l % 8 == 0 or l == args.layers - 1:
-            log(f"layer {l} of {args.layers - 1} extra layers generated and uploaded")
-    vs.temperature, vs.seed = float(args.temperature), int(args.sample_seed)
-    torch.cuda.synchronize()
-    budgets = list(cfg.budgets)
-    state = None
-    if args.state and os.path.exists(args.state):
-        state = json.load(open(args.state))
-        assert state["workload"] == [cfg.cid, args.seed] and state["budgets"] == budgets, "state mismatch"
-        assert state.get("temperature", 0.0) == args.temperature, "state mismatch (temperature)"
-        assert state.get("rs", False) == args.rs, "state mismatch (rs)"
-        assert state.get("layers", 1) == args.layers, "state mismatch (layers)"
-    if args.rs:
-        vs.enable_rs(None)
-        vs.rs_mode = L.RS_HISTORY if args.rs_budget == "history" else L.RS_SCAN
-        vs.k_state.fill_(budgets[-1])
-        log("stochastic drafter: proposals and drafts from the target's own distributions (D passes)")
-        runner.force_drafts_rs_on_device(vs, st["draft"], st["conf"], st["match_u"], args.sample_seed + 1000)
-    elif state is not None:
-        vs.set_draft(np.array(state["draft"], dtype=np.int32))
-        log(f"reusing forced drafts, cost row and dominant kernel from {args.state}")
-    else:
-        log("forcing draft matches (synthetic drafter, D passes at full budget)")
-        runner.force_drafts_on_device(vs, st["draft"], st["conf"], st["match_u"])
-    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda") if args.cold else None
+    budgets = list(cfg.budgets) if not args.force_k else [int(args.force_k)]
+    assert all(cfg.B <= K <= cfg.B * (cfg.D + 1) for K in budgets), "budget outside [B, B(D+1)]"
 
     def timed(fn, reps):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
@@ -317,73 +305,134 @@ def main():
         torch.cuda.synchronize()
         return [a.elapsed_time(b) for a, b in evs]
 
-    # 3. cost row
-    cost_ms, acc_per_k = [], []
-    if state is not None:
-        cost_ms, acc_per_k = state["cost_row_ms"], state["accepted_per_budget"]
-    else:
-        log("cost row: every candidate budget alone")
-    run_step = vs.step_rs if args.rs else vs.step
-    for K in (budgets if state is None else []):
-        step = lambda K=K: run_step([K], [1.0])
-        timed(step, 2)
-        cost_ms.append(statistics.median(timed(step, args.cost_reps)))
-        acc_per_k.append(int(vs.total.item()))
-    log("cost row (ms): " + ", ".join(f"{K}:{c:.3f}" for K, c in zip(budgets, cost_ms)))
-    adaptive = lambda: run_step(budgets, cost_ms)
+    def setup(seed, state):
+        log(f"workload cfg{cfg.cid} ({cfg.name}) seed {seed}: generating")
+        t0 = time.time()
+        st = wl.make_step_inputs(cfg, seed)
+        w = wl.make_weights(cfg, seed)
+        kv = wl.make_kv(cfg, seed, st["ctx_len"])
+        log(f"generated in {time.time() - t0:.1f}s; uploading")
+        vs = runner.VerifyStep(cfg, w, st, kv)
+        for l in range(1, args.layers):
+            vs.add_layer(wl.make_weights(cfg, seed, layer=l), wl.make_kv(cfg, seed, st["ctx_len"], layer=l))
+            if l % 8 == 0 or l == args.layers - 1:
+                log(f"layer {l} of {args.layers - 1} extra layers generated and uploaded")
+        vs.temperature, vs.seed = float(args.temperature), int(args.sample_seed)
+        torch.cuda.synchronize()
+        if args.rs:
+            vs.enable_rs(None)
+            vs.rs_mode = L.RS_HISTORY if args.rs_budget == "history" else L.RS_SCAN
+            vs.k_state.fill_(budgets[-1])
+            log("stochastic drafter: proposals and drafts from the target's own distributions (D passes)")
+            runner.force_drafts_rs_on_device(vs, st["draft"], st["conf"], st["match_u"], args.sample_seed + 1000)
+        elif state is not None:
+            vs.set_draft(np.array(state["draft"], dtype=np.int32))
+            log(f"reusing forced drafts, cost row and dominant kernel from {args.state}")
+        else:
+            log("forcing draft matches (synthetic drafter, D passes at full budget)")
+            runner.force_drafts_on_device(vs, st["draft"], st["conf"], st["match_u"])
+        torch.cuda.synchronize()
+        return vs, st, w, kv
 
-    # 4. per-kernel breakdown with the timing hook
+    def cost_row(vs):
+        """Each candidate budget forced alone (R = 1): median step time and accepted tokens."""
+        run_step = vs.step_rs if args.rs else vs.step
+        cost_ms, acc_per_k = [], []
+        for K in budgets:
+            step = lambda K=K: run_step([K], [1.0])
+            timed(step, 2)
+            cost_ms.append(statistics.median(timed(step, args.cost_reps)))
+            acc_per_k.append(int(vs.total.item()))
+        log("cost row (ms): " + ", ".join(f"{K}:{c:.3f}" for K, c in zip(budgets, cost_ms)))
+        return cost_ms, acc_per_k
+
     names = ["SELECT", "NORM", "GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN",
              "LM_HEAD", "ARGMAX_FINAL"]
     names += ["RS_DECIDE", "RS_RESIDUAL", "RS_FINISH"] if args.rs else ["ACCEPT"]
-    breakdown = {} if state is None else state["kernel_us"]
-    for nm in (names if state is None else []):
-        pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
-        for a, b in pairs:       # create the underlying events
+
+    def kernel_breakdown(fn):
+        """Mean device time (us) of each kernel's last launch in a step, through the timing hook."""
+        out = {}
+        for nm in names:
+            pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+            for a, b in pairs:       # create the underlying events
+                a.record(stream)
+                b.record(stream)
+            torch.cuda.synchronize()
+            for a, b in pairs:
+                L.profile_arm(nm, a, b)
+                fn()
+            L.profile_arm("NONE")
+            torch.cuda.synchronize()
+            out[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
+        return out
+
+    def timed_region(fn, dominant):
+        """`--steps` steps after `--warmup`, bracketed by synchronisations; the dominant kernel of
+        every step timed by events on the launch stream (the library's hook)."""
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for a, b in kev:
             a.record(stream)
             b.record(stream)
         torch.cuda.synchronize()
-        for a, b in pairs:
-            L.profile_arm(nm, a, b)
-            adaptive()
-        L.profile_arm("NONE")
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        breakdown[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
+        start.record(stream)
+        for s in range(args.steps):
+            if flush is not None:
+                flush.fill_(1)
+            L.profile_arm(dominant, kev[s][0], kev[s][1])
+            fn()
+        stop.record(stream)
+        torch.cuda.synchronize()
+        L.profile_arm("NONE")
+        ms = start.elapsed_time(stop) / args.steps
+        return ms, 1000.0 * statistics.mean(a.elapsed_time(b) for a, b in kev)
+
+    # ------------------------------------------------------------ the first seed: the full analysis
+    seed0 = seeds[0]
+    state = None
+    if args.state and os.path.exists(args.state):
+        state = json.load(open(args.state))
+        assert state["workload"] == [cfg.cid, seed0] and state["budgets"] == budgets, "state mismatch"
+        assert state.get("temperature", 0.0) == args.temperature, "state mismatch (temperature)"
+        assert state.get("rs", False) == args.rs, "state mismatch (rs)"
+        assert state.get("layers", 1) == args.layers, "state mismatch (layers)"
+    vs, st, w, kv = setup(seed0, state)
+    run_step = vs.step_rs if args.rs else vs.step
+    if state is not None:
+        cost_ms, acc_per_k = state["cost_row_ms"], state["accepted_per_budget"]
+    elif args.force_k:
+        cost_ms, acc_per_k = [1.0], [0]
+    else:
+        log("cost row: every candidate budget alone")
+        cost_ms, acc_per_k = cost_row(vs)
+    adaptive = lambda: run_step(budgets, cost_ms)
+    breakdown = state["kernel_us"] if state is not None else kernel_breakdown(adaptive)
     # the dominant kernel by time per step: layer kernels launch once per decoder layer
     per_layer = {"GEMM_QKV", "ATTN", "ATTN_COMBINE", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "MOE"}
     dominant = max(breakdown, key=lambda k: breakdown[k] * (args.layers if k in per_layer else 1))
     if args.state and state is None:
-        json.dump(dict(workload=[cfg.cid, args.seed], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,
+        json.dump(dict(workload=[cfg.cid, seed0], budgets=budgets, cost_row_ms=cost_ms, temperature=args.temperature,
                        rs=args.rs, layers=args.layers,
                        accepted_per_budget=acc_per_k, kernel_us=breakdown,
                        draft=vs.host("draft").tolist()), open(args.state, "w"))
     log("kernel us: " + ", ".join(f"{k}={v}" for k, v in breakdown.items()) + f"; dominant {dominant}")
 
-    # 5. timed region
-    for _ in range(args.warmup):
-        adaptive()
-    torch.cuda.synchronize()
-    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    for a, b in kev:
-        a.record(stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    step_ms = []
-    torch.cuda.synchronize()
-    start.record(stream)
-    for s in range(args.steps):
-        if flush is not None:
-            flush.fill_(1)
-        L.profile_arm(dominant, kev[s][0], kev[s][1])
-        adaptive()
-    stop.record(stream)
-    torch.cuda.synchronize()
-    L.profile_arm("NONE")
+    ms_per_step, dom_us = timed_region(adaptive, dominant)
+    Kstar, rstar = vs.host("choice").tolist()
+    accepted = int(vs.total.item())
+    assert int(vs.dev_err.item()) == 0, "device data fault"
+    log(f"seed {seed0}: {ms_per_step:.4f} ms per step, K*={Kstar}, {accepted} accepted")
+    accept_len0 = vs.host("accept_len")
+    draft0 = vs.host("draft")
     # per-step distribution (events around each step, outside the timed region); a
     # profiler replay of saved state runs the timed steps only
     step_dist, cold = None, None
-    if state is None:
+    if state is None and not args.force_k:
         # each step bracketed by events, and its selection kernel timed by the hook (the
         # paper reports the selector's p50/p95 too)
         evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(100)]
@@ -404,7 +453,7 @@ def main():
         step_dist = dict(median_ms=round(statistics.median(per_step), 4), p95_ms=round(per_step[p95], 4),
                          reps=len(per_step), select_median_us=round(statistics.median(sel_us), 2),
                          select_p95_us=round(sel_us[p95], 2))
-    if flush is None and state is None:
+    if flush is None and state is None and not args.force_k:
         # cold cache: a 512 MB write before each step evicts the 256 MB MALL (not timed)
         fl = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
@@ -419,6 +468,24 @@ def main():
         del fl
         log(f"per step: median {step_dist['median_ms']} ms, p95 {step_dist['p95_ms']} ms; "
             f"cold median {cms:.4f} ms")
+    # the unpruned step (K = B(D+1)): per-kernel time and the GEMMs' MFMA rate, where the
+    # verify-layer GEMMs are compute-bound
+    unpruned = None
+    if greedy_headline:
+        Kfull = cfg.B * (cfg.D + 1)
+        full = lambda: vs.step([Kfull], [1.0])
+        ums = statistics.median(timed(full, args.cost_reps))
+        ub = kernel_breakdown(full)
+        gemms = {}
+        for nm in ("GEMM_QKV", "GEMM_O", "GEMM_GATE_UP", "GEMM_DOWN", "LM_HEAD"):
+            fl_, _ = kernel_work(nm, cfg, Kfull, st["ctx_len"])
+            tf = fl_ / (ub[nm] * 1e-6) / 1e12
+            gemms[nm] = dict(us=ub[nm], tflops=round(tf, 1), mfma_frac=round(tf / PEAK_BF16_TFLOPS, 4))
+        ufr = {k: kernel_fraction(k, cfg, Kfull, st["ctx_len"], v) for k, v in ub.items()}
+        unpruned = dict(K=Kfull, ms=round(ums, 4), accepted=int(vs.total.item()), kernel_us=ub, gemm_mfma=gemms,
+                        kernel_roofline={k: v for k, v in ufr.items() if v is not None})
+        log("unpruned step: " + f"{ums:.4f} ms; " + ", ".join(
+            f"{k} {v['us']} us {v['mfma_frac']:.3f} of peak" for k, v in gemms.items()))
     graph = None
     if args.graph:
         g = vs.capture(adaptive)
@@ -442,8 +509,8 @@ def main():
         steps, keep = {}, []
         for Bc in (1, 8, 16, 32, 64):
             c2 = dc.replace(cfg, B=Bc, budgets=tuple(Bc * m for m in range(1, cfg.D + 2)))
-            st2 = wl.make_step_inputs(c2, args.seed)
-            kv2 = wl.make_kv(c2, args.seed, st2["ctx_len"])
+            st2 = wl.make_step_inputs(c2, seed0)
+            kv2 = wl.make_kv(c2, seed0, st2["ctx_len"])
             v2 = runner.VerifyStep(c2, None, st2, kv2, share_weights=vs)
             runner.force_drafts_on_device(v2, st2["draft"], st2["conf"], st2["match_u"])
             graphs = {}
@@ -470,15 +537,28 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    total_ms = start.elapsed_time(stop)
-    ms_per_step = total_ms / args.steps
-    dom_us = 1000.0 * statistics.mean(a.elapsed_time(b) for a, b in kev)
-    Kstar, rstar = vs.host("choice").tolist()
-    accepted = int(vs.total.item())
-    assert int(vs.dev_err.item()) == 0, "device data fault"
-    value = accepted / (ms_per_step * 1e-3)
+    del vs
+    torch.cuda.empty_cache()
 
-    # algorithmic bytes per step (weights, KV read, KV append, packed in/out)
+    # ------------------------------------------------------------ further seeds: the headline protocol
+    per_seed = [dict(seed=seed0, tokens_per_s=round(accepted / (ms_per_step * 1e-3), 1),
+                     ms_per_step=round(ms_per_step, 4), K_star=Kstar, accepted=accepted)]
+    for sd in seeds[1:]:
+        v2, st2, _, _ = setup(sd, None)
+        c2, _ = cost_row(v2)
+        ms2, _ = timed_region(lambda: v2.step(budgets, c2), "NONE")
+        K2 = int(v2.host("choice")[0])
+        acc2 = int(v2.total.item())
+        assert int(v2.dev_err.item()) == 0, "device data fault"
+        per_seed.append(dict(seed=sd, tokens_per_s=round(acc2 / (ms2 * 1e-3), 1), ms_per_step=round(ms2, 4),
+                             K_star=K2, accepted=acc2))
+        log(f"seed {sd}: {ms2:.4f} ms per step, K*={K2}, {acc2} accepted")
+        del v2
+        torch.cuda.empty_cache()
+    med = sorted(per_seed, key=lambda r: r["tokens_per_s"])[len(per_seed) // 2]
+    value = med["tokens_per_s"]
+
+    # algorithmic bytes per step (weights, KV read, KV append, packed in/out) of the first seed
     hd, nkv = ly.head_dim, ly.n_kv
     layer_w = sum(int(w[k].size) * 2 for k in w if k not in ("embed", "w_lm", "final_norm"))
     wbytes = layer_w * args.layers + int(w["w_lm"].size) * 2 + Kstar * ly.hidden * 2
@@ -495,28 +575,30 @@ def main():
     fixed = {}
     for rho, m in (("0.25", 4), ("0.50", 8), ("0.75", 12), ("1.00", 16)):
         K = cfg.B * m
-        if K in budgets:
+        if K in budgets and not args.force_k:
             j = budgets.index(K)
             fixed[rho] = dict(K=K, ms=round(cost_ms[j], 4), accepted=acc_per_k[j],
                               tokens_per_s=round(acc_per_k[j] / (cost_ms[j] * 1e-3), 1))
+    seed_txt = f"median over seeds {seeds[0]}-{seeds[-1]}" if len(seeds) > 1 else f"seed {seed0}"
     out = dict(
         metric="accepted tokens/s of pruned verify step (1 layer + LM head), batch 64; HBM GB/s"
         if args.layers == 1 else
         f"accepted tokens/s of pruned verify step ({args.layers} layers + LM head), batch 64; HBM GB/s",
         value=round(value, 1), unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
-        ms_per_step=round(ms_per_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        ms_per_step=med["ms_per_step"], higher_is_better=True, scaling="weak", vs_baseline=None,
         dtype="bf16", data="synthetic",
         config=dict(workload=f"cfg{cfg.cid} {cfg.name}: B={cfg.B}, D={cfg.D}, H={ly.hidden}, "
                              f"{ly.n_q}q/{ly.n_kv}kv hd{ly.head_dim}, I={ly.inter}, V={ly.vocab}, "
-                             f"L~{cfg.ctx}, conf {cfg.conf_model}; seed {args.seed}",
+                             f"L~{cfg.ctx}, conf {cfg.conf_model}; {seed_txt}",
                     global_batch=cfg.B, K_star=Kstar, r_star=rstar, accepted_per_step=accepted,
-                    layers=args.layers,
+                    layers=args.layers, seeds=seeds,
                     budgets=budgets, parallelism="single GPU", cache="cold" if args.cold else "warm",
                     target_decoding="greedy" if args.temperature == 0 else
                     (f"rejection sampling at temperature {args.temperature} ("
                      + ("causal scan" if args.rs_budget == "scan" else "history-based budget")
                      + f" over shifted scores; seed {args.sample_seed})" if args.rs else
                      f"temperature {args.temperature} (Gumbel-max, seed {args.sample_seed})")),
+        per_seed=per_seed,
         hbm_gbps=round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         step_algorithmic_bytes=int(step_bytes),
         hbm_counted=None if counted is None else dict(
@@ -524,6 +606,7 @@ def main():
         roofline=rl,
         kernel_us=breakdown,
         kernel_roofline=fractions,
+        unpruned=unpruned,
         step_ms=step_dist,
         cold=cold,
         cost_row_ms=[round(c, 4) for c in cost_ms],
@@ -535,8 +618,18 @@ def main():
         out["graph"] = graph
     if table is not None:
         out["cost_table"] = table
-    if not args.no_cpu_baseline and args.temperature == 0 and args.layers == 1:
-        out["cpu_baseline"] = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
+    if not args.no_cpu_baseline and greedy_headline and seed0 == 0:
+        cb = cpu_baseline(cfg, st, w, kv, budgets, cost_ms)
+        # the oracle-forced acceptance of the sampled requests against the GPU's (seed 0, K*)
+        sample = cb.pop("sample_requests")
+        gpu_tokens = int(sum(int(accept_len0[i]) + 1 for i in sample if i not in cb["near_tie_requests"]))
+        cb["gpu_accepted_same_requests"] = gpu_tokens
+        zrows = cb.pop("draft_rows")
+        cb["drafts_equal_gpu_forced"] = int(sum(np.array_equal(zrows[j], draft0[i]) for j, i in enumerate(sample)))
+        log(f"cpu baseline: oracle-forced accepted {cb['oracle_accepted_clear']} vs GPU {gpu_tokens} over "
+            f"{len(sample) - len(cb['near_tie_requests'])} requests")
+        assert cb["oracle_accepted_clear"] == gpu_tokens, "oracle-forced acceptance differs from the GPU step"
+        out["cpu_baseline"] = cb
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

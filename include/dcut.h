@@ -26,10 +26,13 @@
  *     buffer; the library never allocates device memory.  Scratch memory comes
  *     from the caller through (ws, ws_bytes); dcut_workspace_bytes() gives the
  *     size.
- *   - Calls are asynchronous on `stream`, keep no state between calls and never
- *     synchronise the host.  Argument errors a host can see (sizes, limits,
- *     null pointers, budgets, costs) are rejected before any launch with
- *     DCUT_EINVAL or DCUT_EUNSUPPORTED; a failed launch returns DCUT_EHIP.
+ *   - Calls are asynchronous on `stream` and never synchronise the host.  They
+ *     keep no state between calls, with one exception: dcut_profile_arm sets a
+ *     per-thread timing hook that later launches from the same host thread
+ *     honour until it is disarmed (it records events only; results never
+ *     depend on it).  Argument errors a host can see (sizes, limits, null
+ *     pointers, budgets, costs, operand spans) are rejected before any launch
+ *     with DCUT_EINVAL or DCUT_EUNSUPPORTED; a failed launch returns DCUT_EHIP.
  *   - Faults in device-resident data never abort: they OR a DCUT_DERR_* bit
  *     into *dev_err (when dev_err is not NULL) and the affected outputs are
  *     unspecified, but every access stays in bounds.
@@ -212,7 +215,12 @@ typedef struct {
  *   dev_err DCUT_DERR_TOKEN, DCUT_DERR_CAPACITY
  *   ws      dev scratch of dcut_workspace_bytes(1, cfg, B, D) bytes, 256-byte aligned
  * Supported: head_dim in {64, 128}; n_q % n_kv == 0; (n_q / n_kv)(D+1) <= 256;
- * hidden, inter, exp_inter multiples of 8.
+ * hidden, inter, exp_inter multiples of 8; max_ctx * head_dim * 2 bytes (one
+ * request's key or value slab) below 2 GiB; (inter + 256) * hidden * 2 bytes
+ * (the weight rows one gate/up tile spans) below 2 GiB.  Weight matrices of any
+ * total size are addressed per tile.  cu and packed_* must be what
+ * dcut_select wrote (their values are trusted); ctx_len and the cache
+ * descriptor are device data checked as above.
  */
 int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *w, int B, int D,
                       const int32_t *cu, const int32_t *packed_tok, const int32_t *packed_pos,
@@ -237,7 +245,9 @@ int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *w, int B, i
  *   logits   dev [B(D+1)][V] float32 out (nullable, for checking only)
  *   ws       dev scratch of dcut_workspace_bytes(2, cfg with hidden = H and vocab = V,
  *            B, D) bytes, 256-byte aligned
- * Supported: H multiple of 8.
+ * Supported: H multiple of 8, 512 H bytes (one 256-row tile of W) below 2 GiB;
+ * any V (W is addressed per column tile, so weights past 2 GiB are read like
+ * any others).  DCUT_EUNSUPPORTED otherwise, before any launch.
  */
 int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const float *x,
                         const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
@@ -350,7 +360,10 @@ int dcut_nearest_batch(int B, int n, const int32_t *captured);
 /* Kernel timing hook for profilers.  Arms `kernel` (a DCUT_KERNEL_* id) on the
  * calling thread: its next launches on this thread record `start` before and
  * `stop` after the kernel on the launch stream (an id launched several times
- * per call keeps the last launch).  DCUT_KERNEL_NONE disarms.  In a routed-MoE
+ * per call keeps the last launch).  DCUT_KERNEL_NONE disarms.  This is the
+ * library's only state kept between calls: one (kernel, start, stop) triple per
+ * host thread, which changes how the armed kernel is launched (with events)
+ * but never what it computes.  The events must outlive the armed period.  In a routed-MoE
  * layer the grouped expert GEMMs carry the GEMM_GATE_UP and GEMM_DOWN ids and
  * the router, routing, grouping and combine kernels carry MOE. */
 enum {

@@ -149,6 +149,7 @@ struct GemmArgs {
   const int64_t *kv_base;
   const int32_t *kv_cap;
   int n_q, n_kv, head_dim;
+  int n_req;                      // requests in the batch: rows whose packed_req is outside [0, n_req) are skipped
   // EPI_ARGMAX
   unsigned long long *amax_keys;  // [M_max][amax_slots]: per-row maxima of column ranges
   int amax_slots;                 // row stride of amax_keys, at least both gemm_argmax_slots() counts
@@ -188,6 +189,16 @@ __host__ __device__ inline bool lm_head_mid_tile(int M) { return M > 0 && M % 25
 void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid);
 // split-K factor for a residual GEMM of this shape (a function of the shapes, never of K*)
 int gemm_splits(int M_max, int N, int K);
+// Whether the GEMM kernel's 32-bit buffer offsets reach every operand element:
+// a_rows rows of A at stride lda (what one task addresses: a row tile of at
+// most 256 rows, or all of A when rows are gathered) and w_rows rows of W at
+// stride ldw (the span of one column tile: 256 rows, or the SwiGLU split point
+// plus 256 since a tile pairs gate and up rows).  Operands of any total size
+// pass as long as these spans stay below 2 GiB.
+inline bool gemm_span_ok(long long a_rows, long long lda, long long w_rows, long long ldw) {
+  const long long lim = 0x7fffffffLL - 256;
+  return a_rows * lda * 2 < lim && w_rows * ldw * 2 < lim;
+}
 
 // ---------------------------------------------------------------- other launchers
 // x[m] += sum of the split-K partials part[s][m] (in split order), then

@@ -33,6 +33,7 @@
 //   SWIGLU    groups (2p, 2p+1) = (gate rows, up rows) of the same 32 outputs;
 //   QKV_ROPE  groups (2p, 2p+1) = the two halves (j, j + hd/2) of RoPE pairs.
 
+#include <atomic>
 #include <type_traits>
 
 #include "dcut_internal.h"
@@ -135,6 +136,7 @@ __device__ __forceinline__ void qkv_emit(const GemmArgs &a, int gm, int head, in
     q[j + half] = f2bf(o2);
   } else {
     const int req = a.packed_req[gm];
+    if ((unsigned)req >= (unsigned)a.n_req) return;   // not a row of this batch
     const int slot = a.packed_pos[gm];
     const int cap = a.kv_cap[req];
     if (slot < 0 || slot >= cap) return;
@@ -161,7 +163,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
   const int lr = lane / CPR, lc = lane % CPR;
 
   // live tasks: (row tile, split, column tile), row tile fastest
-  const int M = *a.m_count;
+  const int M = min(*a.m_count, a.M_max);
   const int nMT = a.tiles ? *a.n_tiles : (M + TM - 1) / TM;
   const int nNT = n_col_tiles<EPI>(a, TN);
   const int splits = a.splits > 1 ? a.splits : 1;
@@ -171,13 +173,17 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
 
   const int nk_all = (a.K + TK - 1) / TK;
   const int per_split = (nk_all + splits - 1) / splits;
+  // Buffer resources take 32-bit offsets: each task addresses A from its first
+  // row (or, for gathered rows, from the start of A) and W from the first
+  // weight row of its column tile, so the offsets stay below 2^31 for any
+  // operand size the host checks admit (gemm_span_ok).
   const int a_rows_ext = a.a_extent > 0 ? a.a_extent : a.M_max;
-  const long long a_bytes = (long long)a_rows_ext * a.lda * 2;
   const int w_rows_ext = (EPI == EPI_SWIGLU) ? 2 * a.swiglu_inter : a.N;
-  const long long w_bytes = (long long)w_rows_ext * a.ldw * 2;
-  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)a.A, (short)0, (int)(a_bytes < 0x7fffffffLL ? a_bytes : 0x7fffffffLL), 0x00020000);
   constexpr unsigned OOB = 0x80000000u;
+  auto rsrc = [](const uint16_t *base, long long bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0,
+                                             (int)(bytes < 0x7fffffffLL ? bytes : 0x7fffffffLL), 0x00020000);
+  };
 
   // fragment read offsets within a stage (row r at r*TK, chunk swizzled)
   int afrag[WM], bfrag[WN], arx[WM], brx[WN];
@@ -207,8 +213,12 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
       Wb += (size_t)e * a.w_stride;
     }
     const int grp0 = nt * (TN / 32);
-    const __amdgpu_buffer_rsrc_t rsW = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)Wb, (short)0, (int)(w_bytes < 0x7fffffffLL ? w_bytes : 0x7fffffffLL), 0x00020000);
+    // the lowest W row of the tile: its first column group (gate rows precede
+    // up rows; a head's first group is its first 32 dimensions)
+    const int wrow0 = max(group_wrow<EPI>(a, grp0), 0);
+    const __amdgpu_buffer_rsrc_t rsW = rsrc(Wb + (size_t)wrow0 * a.ldw, (long long)(w_rows_ext - wrow0) * a.ldw * 2);
+    const int arow0 = a.a_rows ? 0 : m0;
+    const __amdgpu_buffer_rsrc_t rsA = rsrc(a.A + (size_t)arow0 * a.lda, (long long)(a_rows_ext - arow0) * a.lda * 2);
 
     // Each wave load instruction fills one 1 KB block = 8 rows x 64 k; row r's
     // 16-byte chunk c holds global chunk c ^ swz(r).  Rows past the operand and
@@ -223,7 +233,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
       unsigned off = OOB;
       if (gm < Mlim) {
         const int src = a.a_rows ? a.a_rows[gm] : gm;
-        off = (unsigned)(((long long)src * a.lda + akc[j]) * 2);
+        off = (unsigned)(((long long)(src - arow0) * a.lda + akc[j]) * 2);
       }
       aoff[j] = off;
     }
@@ -236,7 +246,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
       bool ok = wr >= 0;
       if (EPI == EPI_SWIGLU) ok = ok && ((grp >> 1) * 32 + (r & 31)) < a.swiglu_inter;
       else ok = ok && wr + (r & 31) < a.N;
-      boff[j] = ok ? (unsigned)(((long long)(wr + (r & 31)) * a.ldw + bkc[j]) * 2) : OOB;
+      boff[j] = ok ? (unsigned)(((long long)(wr + (r & 31) - wrow0) * a.ldw + bkc[j]) * 2) : OOB;
     }
     auto issueA = [&](int kt, int slot) {
       const int k0 = kt * TK;
@@ -563,7 +573,7 @@ __global__ void __launch_bounds__(Big::THREADS)
 k_gemm_dual(GemmArgs a) {
   static_assert(Mid::THREADS == Big::THREADS && Mid::LDS <= Big::LDS, "one launch shape for both tiles");
   static_assert(MidDeep::THREADS == Big::THREADS && MidDeep::LDS <= Big::LDS, "one launch shape for both tiles");
-  const int M = *a.m_count;
+  const int M = min(*a.m_count, a.M_max);
   if constexpr (EPI == EPI_SWIGLU) {
     // rounds of the persistent grid: a Mid task is half a Big one
     const long long nct = n_col_tiles<EPI>(a, Big::TN), G = gridDim.x;
@@ -614,17 +624,19 @@ k_qkv_reduce(GemmArgs a) {
   qkv_emit(a, m, head, j, x.x, x.y);
 }
 
+// Compute units of the current device, cached per device (atomic: calls from
+// several host threads may fill the cache at once, all with the same value).
 int cu_count() {
-  static int n = 0;
-  if (n == 0) {
-    int dev = 0, c = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0)
-      n = c;
-    else
-      return 256;
+  static std::atomic<int> cached[64];
+  int dev = 0, c = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev >= 0 && dev < 64) {
+    const int n = cached[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
   }
-  return n;
+  if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0) return 256;
+  if (dev >= 0 && dev < 64) cached[dev].store(c, std::memory_order_relaxed);
+  return c;
 }
 
 template <int EPI, class T>

@@ -44,6 +44,15 @@ static bool layer_cfg_supported(const dcut_layer_cfg *c, int B, int D) {
   if (c->head_dim != 64 && c->head_dim != 128) return false;
   if ((c->n_q / c->n_kv) * (D + 1) > 256) return false;
   if (c->n_exp > 0 && !moe_supported(B * (D + 1), c->hidden, c->n_exp, c->top_k)) return false;
+  // 32-bit buffer offsets: one request's key (or value) slab, and each GEMM's spans
+  if ((long long)c->max_ctx * c->head_dim * 2 >= 0x7fffffffLL) return false;
+  const long long H = c->hidden, QD = (long long)c->n_q * c->head_dim;
+  if (!gemm_span_ok(256, H, 256, H) || !gemm_span_ok(256, QD, 256, QD)) return false;
+  if (c->n_exp == 0 && (!gemm_span_ok(256, H, c->inter + 256LL, H) || !gemm_span_ok(256, c->inter, 256, c->inter)))
+    return false;
+  if (c->n_exp > 0 && (!gemm_span_ok((long long)B * (D + 1), H, c->exp_inter + 256LL, H) ||
+                       !gemm_span_ok(256, c->exp_inter, 256, c->exp_inter)))
+    return false;
   return true;
 }
 
@@ -135,7 +144,7 @@ extern "C" int dcut_verify_layer(const dcut_layer_cfg *cfg, const dcut_layer_w *
   g.out_bf16 = q; g.ldo = nq * hd;
   g.packed_pos = packed_pos; g.packed_req = packed_req; g.ctx_len = ctx_len; g.rope_cs = rope;
   g.kv_k = kv->k; g.kv_v = kv->v; g.kv_base = kv->base; g.kv_cap = kv->cap;
-  g.n_q = nq; g.n_kv = nkv; g.head_dim = hd;
+  g.n_q = nq; g.n_kv = nkv; g.head_dim = hd; g.n_req = B;
   g.splits = L.split_qkv; g.split_part = split;
   DCUT_TRY(gemm_launch(DCUT_KERNEL_GEMM_QKV, EPI_QKV_ROPE, g, stream));
   // 3. attention

@@ -96,6 +96,7 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
                        float *logits, float *lse, void *ws, size_t ws_bytes, hipStream_t stream) {
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
   if (!cu || !x || !final_norm || !w_lm || !token || !(eps >= 0.0f)) return DCUT_EINVAL;
+  if (!gemm_span_ok(256, H, 256, H)) return DCUT_EUNSUPPORTED;   // any V: W is addressed per column tile
   const size_t need = lmhead_ws_bytes(H, V, B, D);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);

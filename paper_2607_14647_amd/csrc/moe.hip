@@ -107,14 +107,14 @@ k_moe_route(const float *__restrict__ logits, int E, int k, int M_max, const int
 // One workgroup: sort the K* * k keys (expert << 20 | row * k + slot), then the
 // gather rows, inverse positions and the (expert, first, end) row tiles.
 __global__ void __launch_bounds__(1024)
-k_moe_group(const int32_t *__restrict__ ids, int E, int k, const int32_t *__restrict__ m_count,
+k_moe_group(const int32_t *__restrict__ ids, int E, int k, int M_max, const int32_t *__restrict__ m_count,
             int32_t *__restrict__ row_of, int32_t *__restrict__ inv, int32_t *__restrict__ tiles,
             int32_t *__restrict__ n_tiles) {
   extern __shared__ uint32_t keys[];
   __shared__ int s_cnt[256];
   __shared__ int s_wave[17];
   const int tid = threadIdx.x;
-  const int N = *m_count * k;
+  const int N = min(*m_count, M_max) * k;
   int NP = 64;
   while (NP < N) NP <<= 1;
   for (int j = tid; j < NP; j += blockDim.x) {
@@ -224,7 +224,7 @@ int moe_launch(const MoeArgs &m, hipStream_t s) {
   int NP = 64;
   while (NP < A) NP <<= 1;
   DCUT_TRY(launch(DCUT_KERNEL_MOE, k_moe_group, dim3(1), dim3(1024), (size_t)NP * 4, s, (const int32_t *)ids,
-                  m.E, m.top_k, m.m_count, row_of, inv, tiles, ntiles));
+                  m.E, m.top_k, M, m.m_count, row_of, inv, tiles, ntiles));
   // gathered rows of h through the grouped gate-up GEMM with the SwiGLU epilogue
   GemmArgs gu = {};
   gu.A = m.h; gu.lda = m.H; gu.K = m.H; gu.M_max = A; gu.m_count = m.m_count;

@@ -6,6 +6,10 @@ import sys
 import numpy as np
 import torch
 
+from oracle import accept as oacc
+from oracle import layer as olay
+from oracle import lm_head as olm
+from oracle import select as osel
 from paper_2607_14647_amd import workload as wl
 
 LOGIT_RTOL = 2e-2      # max |l_gpu - l_ref| / max |l_ref| per row (bf16 path vs float64 oracle)
@@ -78,6 +82,72 @@ def workload(cfg: wl.Config, seed: int, with_kv: bool = True):
     w = wl.make_weights(cfg, seed)
     kv = wl.make_kv(cfg, seed, st["ctx_len"]) if with_kv else None
     return st, w, kv
+
+
+@functools.lru_cache(maxsize=1)
+def full_workload(cid: int, seed: int):
+    """A full-size configuration's inputs with the oracle's float64 weights (the last one
+    asked for is kept: several tests share the batch-64 shape)."""
+    cfg = wl.CONFIGS[cid]
+    st = wl.make_step_inputs(cfg, seed)
+    w = wl.make_weights(cfg, seed)
+    kv = wl.make_kv(cfg, seed, st["ctx_len"])
+    return cfg, st, w, kv, olay.prepare_weights(w)
+
+
+def oracle_step(cfg: wl.Config, st, w64, kv, budgets, costs, draft=None, requests=None):
+    """The oracle's whole greedy step: selection, layer and LM head over the kept rows of
+    `requests` (default all), acceptance on the oracle's own argmax."""
+    draft = st["draft"] if draft is None else draft
+    sel = osel.select(st["conf"], draft, st["ctx_len"], list(budgets), list(costs))
+    lay = olay.verify_layer(cfg.layer, w64, kv, sel["cu"], sel["packed_tok"], sel["packed_pos"],
+                            sel["packed_req"], st["ctx_len"], cfg.D, requests=requests)
+    reqs = range(cfg.B) if requests is None else requests
+    rows = np.concatenate([np.arange(sel["cu"][i], sel["cu"][i + 1]) for i in reqs]).astype(np.int64)
+    lm = olm.lm_head_argmax(lay["x_out"][rows], w64["final_norm"], cfg.layer.rms_eps, w64["w_lm"])
+    return dict(sel=sel, lay=lay, lm=lm, rows=rows, draft=draft)
+
+
+def check_step(ref, choice, keep_len, cu, x, argmax, accept_len=None, next_tok=None, logits=None,
+               what=""):
+    """GPU step outputs against oracle_step's: selection and packing bit for bit; residual rows
+    (and logits when given) within their row-relative tolerance on every compared row; argmax
+    where the oracle's top-2 gap exceeds ARGMAX_GAP; acceptance bit for bit for every request
+    whose decisive rows all clear that gap (on the oracle's own argmax).  x, argmax and logits
+    hold the compared rows in the order of ref["rows"]."""
+    sel, lay, lm, rows = ref["sel"], ref["lay"], ref["lm"], ref["rows"]
+    assert np.asarray(choice).tolist() == sel["choice"].tolist(), what
+    assert np.array_equal(keep_len, sel["keep_len"]), what
+    assert np.array_equal(cu, sel["cu"]), what
+    ok = lay["router_gap"][rows] > ROUTER_GAP if "router_gap" in lay else np.ones(len(rows), bool)
+    ex = row_rel_err(np.asarray(x)[ok], lay["x_out"][rows][ok])
+    sure = (lm["gap"] > ARGMAX_GAP) & ok
+    msg = (f"{what}: {len(rows)} rows, {ok.sum()} compared, max rel err x={ex.max(initial=0):.2e}, "
+           f"argmax rows {sure.sum()}")
+    if logits is not None:
+        el = row_rel_err(np.asarray(logits)[ok], lm["logits"][ok])
+        msg += f", logits {el.max(initial=0):.2e}"
+        assert el.max(initial=0) <= LOGIT_RTOL, msg
+    assert ex.max(initial=0) <= X_RTOL, msg
+    assert sure.sum() >= len(rows) // 2, msg
+    assert np.array_equal(np.asarray(argmax)[sure], lm["argmax"][sure]), msg
+    if accept_len is not None:
+        # the oracle's argmax at every compared row; a request is decided when all rows
+        # cu[i] .. cu[i] + min(a_i, n_i) clear the gap
+        g = np.zeros(int(sel["cu"][-1]), dtype=np.int32)
+        g[rows] = lm["argmax"]
+        sure_row = np.zeros(len(g), bool)
+        sure_row[rows] = sure
+        acc = oacc.accept(ref["draft"], sel["keep_len"], sel["cu"], g)
+        B = len(sel["keep_len"])
+        in_rows = np.zeros(len(g), bool)
+        in_rows[rows] = True
+        decided = np.array([in_rows[sel["cu"][i]] and
+                            sure_row[sel["cu"][i]: sel["cu"][i] + acc["accept_len"][i] + 1].all() for i in range(B)])
+        msg += f", acceptance decided for {decided.sum()}/{B} requests"
+        assert np.array_equal(np.asarray(accept_len)[decided], acc["accept_len"][decided]), msg
+        assert np.array_equal(np.asarray(next_tok)[decided], acc["next_tok"][decided]), msg
+    note(msg)
 
 
 def row_rel_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:

@@ -162,3 +162,25 @@ def test_other_entry_points_reject_invalid_args():
     assert lib.dcut_profile_arm(L.KERNELS["LM_HEAD"], None, None) == L.EINVAL
     assert lib.dcut_profile_arm(0, None, None) == L.OK
     assert L.strerror(L.EHIP).startswith("HIP")
+
+
+def test_operands_past_32bit_offsets_are_rejected_before_any_launch():
+    """The GEMM addresses each task's A rows and each column tile's W rows from their own
+    base, so any total weight size is accepted (an LM head of H = 8192, V = 152064, 2.49 GB,
+    passes validation and fails only on the fake workspace); what a single task or column
+    tile spans must stay below 2 GiB, else DCUT_EUNSUPPORTED before any launch."""
+    lib = L.lib()
+    fake = C.c_void_p(0x1000)
+    lm = lambda H, V: lib.dcut_lm_head_argmax(H, V, 4, 15, fake, fake, fake, 1e-5, fake, fake, None, None,
+                                              None, 0, None)
+    assert lm(8192, 152064) == L.EWORKSPACE
+    assert lm(1 << 22, 1024) == L.EUNSUPPORTED         # one 256-row tile of W spans 2 GiB
+    w = L.LayerW(*([0x1000] * 7 + [None] * 3))
+    kv = L.KV(0x1000, 0x1000, 0x1000, 0x1000)
+    call = lambda c: lib.dcut_verify_layer(C.byref(c), C.byref(w), 4, 15, fake, fake, fake, fake, fake, None,
+                                           C.byref(kv), fake, None, None, 0, None)
+    # a SwiGLU tile pairs gate row p with up row inter + p: inter * hidden * 2 bytes apart
+    assert call(L.LayerCfg(8192, 64, 8, 128, 1 << 17, 0, 0, 0, 1024, 160, 1e-5, 5e5)) == L.EUNSUPPORTED
+    assert call(L.LayerCfg(8192, 64, 8, 128, 28672, 0, 0, 0, 1024, 160, 1e-5, 5e5)) == L.EWORKSPACE
+    # one request's key slab [cap][head_dim] must stay below 2 GiB
+    assert call(L.LayerCfg(256, 4, 2, 128, 688, 0, 0, 0, 1024, 1 << 23, 1e-5, 5e5)) == L.EUNSUPPORTED
