@@ -23,6 +23,15 @@ their internals, so the layer follows the usual Llama/Qwen form:
 All arithmetic is float64 on the exact bf16 values of weights and cache.
 `row_exact=True` evaluates every product one row at a time with the same
 shapes, so a row's result cannot depend on which other rows are present.
+
+`act_bf16=True` is the same definition with the tensors the verify step
+holds in bf16 between its operations rounded to bf16 (nearest even) where
+they are formed: the normalised rows h and h2, q after RoPE, the keys and
+values appended to the (bf16) cache, the attention output and the SwiGLU
+product.  Everything else stays float64.  The argmax is an integer decided
+by floating point, so the tests take that decision on logits formed from the
+same bf16 activations as the path under test (the logit and residual
+tolerances are still checked against the plain float64 forward).
 """
 from __future__ import annotations
 
@@ -45,6 +54,15 @@ def prepare_weights(w: Dict[str, np.ndarray]) -> Dict[str, np.ndarray]:
     for name, arr in w.items():
         out[name] = arr if name == "embed" else bf16_bits_to_f64(arr)
     return out
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Nearest bf16 value (ties to even) of float64 values, as float64: first to float32
+    (the precision the activations are formed in), then to the 8-bit significand."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64).reshape(np.shape(x))
 
 
 def rmsnorm(x: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
@@ -115,13 +133,14 @@ def verify_layer(ly, w64: Dict[str, np.ndarray], kv: Dict[str, np.ndarray],
                  packed_req: np.ndarray, ctx_len: np.ndarray, D: int,
                  x_in: Optional[np.ndarray] = None,
                  requests: Optional[Sequence[int]] = None,
-                 row_exact: bool = False) -> Dict[str, np.ndarray]:
+                 row_exact: bool = False, act_bf16: bool = False) -> Dict[str, np.ndarray]:
     """Layer forward over the packed rows of `requests` (default: all).
 
     Returns x_out [K*][H] (rows of other requests are NaN), the appended keys
     (after RoPE) and values new_k/new_v [K*][n_kv][hd], and, for MoE layers,
     router probabilities/ids per row."""
     H, nq, nkv, hd = ly.hidden, ly.n_q, ly.n_kv, ly.head_dim
+    act = round_bf16 if act_bf16 else (lambda a: a)
     B = len(ctx_len)
     Kstar = int(cu[B])
     x_out = np.full((Kstar, H), np.nan)
@@ -145,24 +164,24 @@ def verify_layer(ly, w64: Dict[str, np.ndarray], kv: Dict[str, np.ndarray],
             if (tok < 0).any() or (tok >= ly.vocab).any():
                 raise DcutDataError(DERR_TOKEN, f"request {i}: token out of range")
             x = bf16_bits_to_f64(w64["embed"][tok])
-        h = rmsnorm(x, w64["attn_norm"], ly.rms_eps)
+        h = act(rmsnorm(x, w64["attn_norm"], ly.rms_eps))
         qkv = _mm(h, w64["w_qkv"], row_exact).reshape(d, nq + 2 * nkv, hd)
         pos = packed_pos[t0:t1].astype(np.float64)
-        q = rope(qkv[:, :nq], pos[:, None], ly.rope_theta)
-        kb = rope(qkv[:, nq:nq + nkv], pos[:, None], ly.rope_theta)
-        vb = qkv[:, nq + nkv:]
+        q = act(rope(qkv[:, :nq], pos[:, None], ly.rope_theta))
+        kb = act(rope(qkv[:, nq:nq + nkv], pos[:, None], ly.rope_theta))
+        vb = act(qkv[:, nq + nkv:])
         base = int(kv["base"][i])
         slab = nkv * cap * hd
         ck = bf16_bits_to_f64(kv["k"][base: base + slab]).reshape(nkv, cap, hd)[:, :L]
         cv = bf16_bits_to_f64(kv["v"][base: base + slab]).reshape(nkv, cap, hd)[:, :L]
         k_all = np.concatenate([ck, kb.transpose(1, 0, 2)], axis=1)
         v_all = np.concatenate([cv, vb.transpose(1, 0, 2)], axis=1)
-        att = attention(q, k_all, v_all, L).reshape(d, nq * hd)
+        att = act(attention(q, k_all, v_all, L).reshape(d, nq * hd))
         y = x + _mm(att, w64["w_o"], row_exact)
-        h2 = rmsnorm(y, w64["mlp_norm"], ly.rms_eps)
+        h2 = act(rmsnorm(y, w64["mlp_norm"], ly.rms_eps))
         if not moe:
             gu = _mm(h2, w64["w_gate_up"], row_exact)
-            m = silu(gu[:, : ly.inter]) * gu[:, ly.inter:]
+            m = act(silu(gu[:, : ly.inter]) * gu[:, ly.inter:])
             out = y + _mm(m, w64["w_down"], row_exact)
         else:
             logits = _mm(h2, w64["w_router"], row_exact)
@@ -174,7 +193,7 @@ def verify_layer(ly, w64: Dict[str, np.ndarray], kv: Dict[str, np.ndarray],
                 for slot in range(ly.top_k):
                     e = int(ids[r, slot])
                     gu = w64["w_exp_gate_up"][e] @ h2[r]
-                    m = silu(gu[:Ie]) * gu[Ie:]
+                    m = act(silu(gu[:Ie]) * gu[Ie:])
                     acc += wts[r, slot] * (w64["w_exp_down"][e] @ m)
                 out[r] += acc
             r_ids[t0:t1] = ids

@@ -226,3 +226,44 @@ def test_forced_drafts_accept_as_constructed():
     for i in range(B):
         first_miss = int(np.argmin(np.append(hit[i], False)))
         assert acc["accept_len"][i] >= first_miss
+
+
+def test_round_bf16_matches_torch_bfloat16():
+    """The oracle's bf16 rounding (float64 -> float32 -> nearest even bf16) equals torch's
+    float32 -> bfloat16 conversion, ties included."""
+    import torch
+    rng = np.random.default_rng(5)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [0.0, -0.0, 1.0, -1.5, 3.0e38, -3.0e38, 1e-40]])
+    # exact ties: float32 values whose low 16 bits are 0x8000, with even and odd bf16 neighbours
+    ties = (np.arange(0x3F800000, 0x3F800000 + 64 * 0x10000, 0x10000, dtype=np.uint32) + 0x8000).view(np.float32)
+    x = np.concatenate([x, ties.astype(np.float64), -ties.astype(np.float64)])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    got = olay.round_bf16(x)
+    assert np.array_equal(got, ref)
+    assert np.array_equal(olay.round_bf16(got), got)          # idempotent
+
+
+def test_bf16_activation_mode_rounds_only_where_stated():
+    """act_bf16 changes the forward only by bf16 roundings of the stored activations: the
+    appended keys and values come out bf16-representable, the results stay within a few
+    bf16 ulps of the float64 forward (relative to the row), and they are not identical."""
+    cfg = wl.CONFIGS[1]
+    st = wl.make_step_inputs(cfg, 0)
+    w = wl.make_weights(cfg, 0)
+    kv = wl.make_kv(cfg, 0, st["ctx_len"])
+    sel = osel.select(st["conf"], st["draft"], st["ctx_len"], [40], [1.0])
+    w64 = olay.prepare_weights(w)
+    args = (cfg.layer, w64, kv, sel["cu"], sel["packed_tok"], sel["packed_pos"], sel["packed_req"],
+            st["ctx_len"], cfg.D)
+    ref = olay.verify_layer(*args)
+    got = olay.verify_layer(*args, act_bf16=True)
+    for name in ("new_k", "new_v"):
+        assert np.array_equal(olay.round_bf16(got[name]), got[name])
+        assert np.abs(got[name] - ref[name]).max() <= 2.0 ** -8 * np.abs(ref[name]).max()
+    rel = np.abs(got["x_out"] - ref["x_out"]).max(axis=1) / np.abs(ref["x_out"]).max(axis=1)
+    assert 0 < rel.max() < 2e-2
+    lm = olm.lm_head_argmax(ref["x_out"], w64["final_norm"], cfg.layer.rms_eps, w64["w_lm"])
+    lm16 = olm.lm_head_argmax(got["x_out"], w64["final_norm"], cfg.layer.rms_eps, w64["w_lm"], act_bf16=True)
+    rl = np.abs(lm16["logits"] - lm["logits"]).max(axis=1) / np.abs(lm["logits"]).max(axis=1)
+    assert 0 < rl.max() < 2e-2
