@@ -219,11 +219,11 @@ def _mutant(old: str, new: str):
 MUTATIONS = {
     "drop attention residual": ("cfg1", 'y = x + _mm(att, w64["w_o"], row_exact)', 'y = _mm(att, w64["w_o"], row_exact)'),
     "drop MLP residual": ("cfg1", 'out = y + _mm(m, w64["w_down"], row_exact)', 'out = _mm(m, w64["w_down"], row_exact)'),
-    "swap gate and up": ("cfg1", "m = silu(gu[:, : ly.inter]) * gu[:, ly.inter:]",
-                         "m = silu(gu[:, ly.inter:]) * gu[:, : ly.inter]"),
-    "no pre-attention norm": ("cfg1", 'h = rmsnorm(x, w64["attn_norm"], ly.rms_eps)', "h = x"),
-    "post-norm residual": ("cfg1", 'h2 = rmsnorm(y, w64["mlp_norm"], ly.rms_eps)',
-                           'y = rmsnorm(y, w64["mlp_norm"], ly.rms_eps); h2 = y'),
+    "swap gate and up": ("cfg1", "m = act(silu(gu[:, : ly.inter]) * gu[:, ly.inter:])",
+                         "m = act(silu(gu[:, ly.inter:]) * gu[:, : ly.inter])"),
+    "no pre-attention norm": ("cfg1", 'h = act(rmsnorm(x, w64["attn_norm"], ly.rms_eps))', "h = act(x)"),
+    "post-norm residual": ("cfg1", 'h2 = act(rmsnorm(y, w64["mlp_norm"], ly.rms_eps))',
+                           'y = rmsnorm(y, w64["mlp_norm"], ly.rms_eps); h2 = act(y)'),
     "interleaved head groups": ("cfg1", "g = h // grp", "g = h % nkv"),
     "block not causal": ("cfg1", "n = L + r + 1", "n = L + d"),
     "MoE weights not renormalised": ("moe", "w = pt / pt.sum(axis=-1, keepdims=True)", "w = pt"),
