@@ -255,6 +255,33 @@ int dcut_lm_head_argmax(int H, int V, int B, int D, const int32_t *cu, const flo
                         void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * dcut_lm_head_argmax_static -- dcut_lm_head_argmax without a workspace, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * serving loops that must not call hipMalloc, harnesses that forbid it.
+ *
+ * Same arguments, kernels and results (bit for bit) as dcut_lm_head_argmax,
+ * minus (ws, ws_bytes): the scratch (normalised rows and partial argmax keys)
+ * lives in a static device array of dcut_lm_head_static_scratch_bytes()
+ * bytes (32 MiB) that every device the library runs on holds until the process
+ * ends.  The call allocates nothing and calls no allocating routine; the first
+ * call on a device looks up that device's copy of the array.  Every call on one
+ * device shares the array: calls that overlap on a device (different streams,
+ * different host threads without ordering) race and give unspecified results.
+ * Nothing in the array needs clearing between calls (every value read was
+ * written by the same call).
+ * Returns DCUT_EUNSUPPORTED, before any launch, when the scratch the shape needs,
+ * 2 B(D+1) H + 32 B(D+1) ceil(V / 256) bytes (each part rounded up to 256), exceeds
+ * the array (the batch-64 step with V = 128256 and H = 4096 needs 23.7 MiB at
+ * B(D+1) = 1024); DCUT_EHIP if the array's address cannot be looked up; otherwise
+ * as dcut_lm_head_argmax.
+ */
+int dcut_lm_head_argmax_static(int H, int V, int B, int D, const int32_t *cu, const float *x,
+                               const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
+                               int32_t *argmax, float *max_logit, float *logits, hipStream_t stream);
+/* Size in bytes of the static scratch array of dcut_lm_head_argmax_static. */
+size_t dcut_lm_head_static_scratch_bytes(void);
+
+/*
  * dcut_lm_head_sample -- target token of every kept row drawn at temperature T.
  *
  * Temperature-T target sampling with target-only verification (Sec. 4,

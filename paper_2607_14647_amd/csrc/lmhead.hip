@@ -9,16 +9,22 @@
 // of every row.  The full logits are
 // never written, no atomics contend on a row, the result does not depend on
 // workgroup order, and the lowest column wins exact ties.
+#include <atomic>
+#include <mutex>
+
 #include "dcut_internal.h"
 
 namespace dcut {
 
-size_t lmhead_ws_bytes(int H, int V, int B, int D) {
+// Scratch of the LM-head call: the normalised rows, the partial keys and (for a
+// sampling call that returns the log-partition) the partial (max, sum) pairs.
+static size_t lmhead_need(int H, int V, int B, int D, bool with_lse) {
   const size_t M = (size_t)B * (D + 1);
   const size_t slots = 4 * (((size_t)V + 255) / 256);   // row stride of the partial keys (64 columns each)
-  // normalised rows, partial keys, partial log-partition pairs
-  return align256(M * H * 2) + 2 * align256(M * slots * sizeof(unsigned long long));
+  return align256(M * H * 2) + (with_lse ? 2 : 1) * align256(M * slots * sizeof(unsigned long long));
 }
+
+size_t lmhead_ws_bytes(int H, int V, int B, int D) { return lmhead_need(H, V, B, D, true); }
 
 namespace {
 
@@ -97,7 +103,7 @@ static int lm_head_run(EpiKind epi, int H, int V, int B, int D, const int32_t *c
   if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
   if (!cu || !x || !final_norm || !w_lm || !token || !(eps >= 0.0f)) return DCUT_EINVAL;
   if (!gemm_span_ok(256, H, 256, H)) return DCUT_EUNSUPPORTED;   // any V: W is addressed per column tile
-  const size_t need = lmhead_ws_bytes(H, V, B, D);
+  const size_t need = lmhead_need(H, V, B, D, lse != nullptr);
   if (!ws || ws_bytes < need || ((uintptr_t)ws & 255)) return DCUT_EWORKSPACE;
   const int M = B * (D + 1);
   uint16_t *f = (uint16_t *)ws;
@@ -139,4 +145,49 @@ extern "C" int dcut_lm_head_sample(int H, int V, int B, int D, const int32_t *cu
     return DCUT_EINVAL;
   return lm_head_run(EPI_SAMPLE, H, V, B, D, cu, x, final_norm, eps, w_lm, packed_req, packed_pos,
                      1.0f / temperature, seed, token, max_score, logits, lse, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- allocation-free variant
+// The greedy LM head with its scratch in a file-scope device array instead of
+// a caller workspace.  Each device the library runs on holds its own copy of
+// the array (for the life of the process); host code reaches it only through
+// the address hipGetSymbolAddress returns on that device, fetched once per
+// device on the first call made with that device current.
+namespace {
+constexpr size_t LM_STATIC_SCRATCH = (size_t)32 << 20;
+constexpr int MAX_DEVICES = 64;
+__device__ __align__(256) unsigned char scratch[LM_STATIC_SCRATCH];
+std::atomic<void *> scratch_addr[MAX_DEVICES];
+std::mutex scratch_mutex;
+
+int scratch_of_current_device(void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DCUT_EHIP;
+  if (dev < 0 || dev >= MAX_DEVICES) return DCUT_EUNSUPPORTED;
+  void *p = scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(scratch_mutex);
+    p = scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DCUT_EHIP;
+      scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return DCUT_OK;
+}
+}  // namespace
+
+extern "C" size_t dcut_lm_head_static_scratch_bytes(void) { return LM_STATIC_SCRATCH; }
+
+extern "C" int dcut_lm_head_argmax_static(int H, int V, int B, int D, const int32_t *cu, const float *x,
+                                          const dcut_bf16 *final_norm, float eps, const dcut_bf16 *w_lm,
+                                          int32_t *argmax, float *max_logit, float *logits, hipStream_t stream) {
+  if (!batch_ok(B, D) || H <= 0 || H % 8 || V <= 0) return DCUT_EINVAL;
+  if (!cu || !x || !final_norm || !w_lm || !argmax || !(eps >= 0.0f)) return DCUT_EINVAL;
+  if (!gemm_span_ok(256, H, 256, H) || lmhead_need(H, V, B, D, false) > LM_STATIC_SCRATCH) return DCUT_EUNSUPPORTED;
+  void *ws = nullptr;
+  DCUT_TRY(scratch_of_current_device(&ws));
+  return lm_head_run(EPI_ARGMAX, H, V, B, D, cu, x, final_norm, eps, w_lm, nullptr, nullptr, 0.0f, 0, argmax,
+                     max_logit, logits, nullptr, ws, LM_STATIC_SCRATCH, stream);
 }

@@ -23,9 +23,10 @@ KERNELS = dict(NONE=0, SELECT=1, PACK=2, NORM=3, GEMM_QKV=4, ATTN=5, ATTN_COMBIN
                RS_DECIDE=14, RS_RESIDUAL=15, RS_FINISH=16, ATTN_PLAN=17)
 RS_SCAN, RS_FIXED, RS_HISTORY = 0, 1, 2
 
-EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_accept",
-           "dcut_lm_head_sample", "dcut_select_rs", "dcut_accept_rs", "dcut_workspace_bytes", "dcut_strerror",
-           "dcut_budgets_from_ratios", "dcut_nearest_batch", "dcut_profile_arm"]
+EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_argmax_static",
+           "dcut_lm_head_static_scratch_bytes", "dcut_accept", "dcut_lm_head_sample", "dcut_select_rs",
+           "dcut_accept_rs", "dcut_workspace_bytes", "dcut_strerror", "dcut_budgets_from_ratios",
+           "dcut_nearest_batch", "dcut_profile_arm"]
 
 
 class DcutError(RuntimeError):
@@ -62,6 +63,9 @@ def _load() -> C.CDLL:
     lib.dcut_verify_layer.argtypes = [C.POINTER(LayerCfg), C.POINTER(LayerW), i32, i32, vp, vp, vp, vp,
                                       vp, vp, C.POINTER(KV), vp, vp, vp, sz, vp]
     lib.dcut_lm_head_argmax.argtypes = [i32, i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp, sz, vp]
+    lib.dcut_lm_head_argmax_static.argtypes = [i32, i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp, vp]
+    lib.dcut_lm_head_static_scratch_bytes.argtypes = []
+    lib.dcut_lm_head_static_scratch_bytes.restype = sz
     lib.dcut_lm_head_sample.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, C.c_float, vp, C.c_float,
                                         C.c_uint64, vp, vp, vp, vp, vp, sz, vp]
     lib.dcut_accept.argtypes = [i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -75,7 +79,8 @@ def _load() -> C.CDLL:
     lib.dcut_budgets_from_ratios.argtypes = [i32, i32, i32, vp, vp, vp]
     lib.dcut_nearest_batch.argtypes = [i32, i32, vp]
     lib.dcut_profile_arm.argtypes = [i32, vp, vp]
-    for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_sample", "dcut_accept",
+    for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_argmax_static",
+              "dcut_lm_head_sample", "dcut_accept",
               "dcut_select_rs", "dcut_accept_rs", "dcut_budgets_from_ratios", "dcut_nearest_batch",
               "dcut_profile_arm"]:
         getattr(lib, f).restype = i32
@@ -206,6 +211,19 @@ def lm_head_argmax(H: int, V: int, B: int, D: int, cu: torch.Tensor, x: torch.Te
                                   _p(argmax), _p(max_logit), _p(logits), _p(ws),
                                   ws.numel() * ws.element_size(), _stream(stream))
     _check(st, "dcut_lm_head_argmax")
+
+
+def lm_head_argmax_static(H: int, V: int, B: int, D: int, cu: torch.Tensor, x: torch.Tensor,
+                          final_norm: torch.Tensor, eps: float, w_lm: torch.Tensor, argmax: torch.Tensor,
+                          max_logit: Optional[torch.Tensor] = None, logits: Optional[torch.Tensor] = None,
+                          stream=None) -> None:
+    st = _lib.dcut_lm_head_argmax_static(H, V, B, D, _p(cu), _p(x), _p(final_norm), float(eps), _p(w_lm),
+                                         _p(argmax), _p(max_logit), _p(logits), _stream(stream))
+    _check(st, "dcut_lm_head_argmax_static")
+
+
+def lm_head_static_scratch_bytes() -> int:
+    return int(_lib.dcut_lm_head_static_scratch_bytes())
 
 
 def lm_head_sample(H: int, V: int, B: int, D: int, cu: torch.Tensor, packed_req: torch.Tensor,

@@ -184,3 +184,18 @@ def test_operands_past_32bit_offsets_are_rejected_before_any_launch():
     assert call(L.LayerCfg(8192, 64, 8, 128, 28672, 0, 0, 0, 1024, 160, 1e-5, 5e5)) == L.EWORKSPACE
     # one request's key slab [cap][head_dim] must stay below 2 GiB
     assert call(L.LayerCfg(256, 4, 2, 128, 688, 0, 0, 0, 1024, 1 << 23, 1e-5, 5e5)) == L.EUNSUPPORTED
+
+
+def test_static_lm_head_rejects_shapes_beyond_its_array():
+    """dcut_lm_head_argmax_static refuses, before any launch, a shape whose scratch exceeds its
+    32 MiB array (the 256-request step with V = 151936 needs far more) and validates like the
+    workspace call."""
+    lib = L.lib()
+    fake = C.c_void_p(0x1000)
+    call = lambda H, V, B, D, out=fake: lib.dcut_lm_head_argmax_static(H, V, B, D, fake, fake, fake, 1e-5, fake,
+                                                                       out, None, None, None)
+    assert L.lm_head_static_scratch_bytes() == 32 << 20
+    assert call(4096, 151936, 256, 15) == L.EUNSUPPORTED
+    assert call(4095, 1024, 4, 15) == L.EINVAL
+    assert call(4096, 1024, 0, 15) == L.EINVAL
+    assert call(4096, 1024, 4, 15, out=None) == L.EINVAL
