@@ -47,20 +47,25 @@ constexpr int TK = 64;       // k per LDS stage: one 128-byte row per operand ro
 constexpr int CPR = TK / 8;  // 16-byte chunks per row
 constexpr int RPI = 64 / CPR;  // rows per 1 KB wave load
 
-template <int GM_, int GN_, int WM_, int WN_, int NA_ = 2, int NB_ = 3>
+template <int GM_, int GN_, int WM_, int WN_, int NA_ = 2, int NB_ = 3, bool SKEW_ = false>
 struct Tile {
   static constexpr int GM = GM_, GN = GN_, WM = WM_, WN = WN_;
+  static constexpr bool SKEW = SKEW_;   // second half of the waves two sub-steps behind (8-wave tiles)
   static constexpr int NWV = GM * GN, THREADS = 64 * NWV;
   static constexpr int TM = GM * WM * 32, TN = GN * WN * 32;
-  static constexpr int NA = NA_, NB = NB_;   // ring stages of A and W (NA = 2, NB = 3 or 4)
-  static_assert(NA == 2 && (NB == 3 || NB == 4), "ring depths the wait counts are written for");
+  // ring stages of A and W: slice it + NA - 1 of A and it + NB - 1 of W are
+  // requested while slice it is multiplied
+  static constexpr int NA = NA_, NB = NB_;
+  static_assert(NA >= 2 && NB >= 2, "double buffering at least");
   static constexpr size_t LDS = (size_t)(NA * TM + NB * TN) * TK * sizeof(uint16_t);
+  static_assert(LDS <= 163840, "the LDS of one CU");
   static constexpr int PER_CU = LDS > 81920 ? 1 : 2;
 };
-using Big = Tile<4, 2, 2, 4>;
-using Mid = Tile<2, 4, 2, 2>;     // 128 x 256, eight waves in a 2 x 4 grid, 128 KB
+using Big = Tile<4, 2, 2, 4, 2, 3, true>;
+using Mid = Tile<2, 4, 2, 2, 2, 3, true>;     // 128 x 256, eight waves in a 2 x 4 grid, 128 KB
 using Small = Tile<2, 2, 2, 2>;
-using MidDeep = Tile<2, 4, 2, 2, 2, 4>;   // 128 x 256 with four W slices: the LM head at few live rows
+using MidDeep = Tile<2, 4, 2, 2, 2, 4, true>;   // 128 x 256 with four W slices: the LM head at few live rows
+using BigFlat = Tile<4, 2, 2, 4>;   // Big without the skew: the sampling epilogue needs its registers
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -84,6 +89,43 @@ template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt is six bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// s_waitcnt with the largest immediate in [LO, HI] that is at most n (n >= LO):
+// a binary search over immediates, since vmcnt cannot come from a register.
+template <int LO, int HI>
+__device__ __forceinline__ void wait_vm_le(int n) {
+  if constexpr (LO == HI) {
+    wait_vm<LO>();
+  } else {
+    constexpr int MID = (LO + HI + 1) / 2;
+    if (n >= MID) wait_vm_le<MID, HI>(n);
+    else wait_vm_le<LO, MID - 1>(n);
+  }
+}
+
+// Vector-memory loads that may still be outstanding when iteration `it` of a
+// k loop of nk slices needs its A and W slices.  Issue order: prologue groups
+// j = 0 .. P-1 (A[j] if j < PA, then W[j] if j < PW), then one group per
+// iteration i (A[i + PA], then W[i + PW]); slices at or past nk are never
+// issued; AJ and BJ are the load instructions of one A and one W slice.  The
+// loads issued after the later of A[it] and W[it] may be outstanding.
+template <int PA, int PW, int AJ, int BJ>
+__device__ __forceinline__ int loads_after(int it, int nk) {
+  constexpr int P = PA > PW ? PA : PW;
+  const int gA = it < PA ? it : P + it - PA;
+  const int gW = it < PW ? it : P + it - PW;
+  const bool last_is_a = gA > gW;          // in a shared group W follows A
+  const int g = last_is_a ? gA : gW;
+  auto has_a = [&](int q) { return q < P ? (q < PA && q < nk) : (q - P + PA < nk); };
+  auto has_w = [&](int q) { return q < P ? (q < PW && q < nk) : (q - P + PW < nk); };
+  int n = (last_is_a && has_w(g)) ? BJ : 0;
+#pragma unroll
+  for (int d = 1; d <= P; ++d) {
+    const int q = g + d;
+    if (q < P + it) n += (has_a(q) ? AJ : 0) + (has_w(q) ? BJ : 0);
+  }
+  return n;
 }
 
 // W row feeding logical tile column group `grp` (global, 32 columns each);
@@ -157,7 +199,9 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
   uint16_t *const ldsA = lds;
   uint16_t *const ldsW = lds + NA * TM * TK;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: kept in a scalar register, so LDS destinations
+  // of the operand loads are scalar arithmetic
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / GN, wn = wave % GN;
   const int l32 = lane & 31, kh = lane >> 5;
   const int lr = lane / CPR, lc = lane % CPR;
@@ -224,48 +268,53 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
     // 16-byte chunk c holds global chunk c ^ swz(r).  Rows past the operand and
     // k past K get an offset beyond the buffer, which reads as zeros.
     unsigned aoff[AJ], boff[BJ];
-    int akc[AJ], bkc[BJ];
+    // k chunk (elements) that load j of this lane fetches within a 64-k slice
+    auto kchunk = [&](int j) { return 8 * (lc ^ swz(RPI * (wave + NWV * j) + lr)); };
 #pragma unroll
     for (int j = 0; j < AJ; ++j) {
       const int r = RPI * (wave + NWV * j) + lr;
-      akc[j] = 8 * (lc ^ swz(r));
       const int gm = m0 + r;
       unsigned off = OOB;
       if (gm < Mlim) {
         const int src = a.a_rows ? a.a_rows[gm] : gm;
-        off = (unsigned)(((long long)(src - arow0) * a.lda + akc[j]) * 2);
+        off = (unsigned)(((long long)(src - arow0) * a.lda + kchunk(j)) * 2);
       }
       aoff[j] = off;
     }
 #pragma unroll
     for (int j = 0; j < BJ; ++j) {
       const int r = RPI * (wave + NWV * j) + lr;
-      bkc[j] = 8 * (lc ^ swz(r));
       const int grp = grp0 + (r >> 5);
       const int wr = group_wrow<EPI>(a, grp);
       bool ok = wr >= 0;
       if (EPI == EPI_SWIGLU) ok = ok && ((grp >> 1) * 32 + (r & 31)) < a.swiglu_inter;
       else ok = ok && wr + (r & 31) < a.N;
-      boff[j] = ok ? (unsigned)(((long long)(wr + (r & 31) - wrow0) * a.ldw + bkc[j]) * 2) : OOB;
+      boff[j] = ok ? (unsigned)(((long long)(wr + (r & 31) - wrow0) * a.ldw + kchunk(j)) * 2) : OOB;
     }
+    // The k offset of a slice goes in the scalar offset; the per-lane offsets
+    // stay fixed over the k loop.  Rows past the operand carry OOB, which stays
+    // beyond the buffer with any scalar offset added.  Only a slice reaching
+    // past K (K not a multiple of TK) masks its chunks beyond K lane by lane.
     auto issueA = [&](int kt, int slot) {
       const int k0 = kt * TK;
       uint16_t *sa = ldsA + slot * (TM * TK);
+      const bool tail = k0 + TK > a.K;
 #pragma unroll
       for (int j = 0; j < AJ; ++j) {
-        const unsigned off = (aoff[j] != OOB && k0 + akc[j] < a.K) ? aoff[j] + (unsigned)k0 * 2 : OOB;
+        const unsigned off = (tail && k0 + kchunk(j) >= a.K) ? OOB : aoff[j];
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (__attribute__((address_space(3))) void *)(sa + (wave + NWV * j) * 512),
-                                                 16, off, 0, 0, 0);
+                                                 16, off, k0 * 2, 0, 0);
       }
     };
     auto issueW = [&](int kt, int slot) {
       const int k0 = kt * TK;
       uint16_t *sb = ldsW + slot * (TN * TK);
+      const bool tail = k0 + TK > a.K;
 #pragma unroll
       for (int j = 0; j < BJ; ++j) {
-        const unsigned off = (boff[j] != OOB && k0 + bkc[j] < a.K) ? boff[j] + (unsigned)k0 * 2 : OOB;
+        const unsigned off = (tail && k0 + kchunk(j) >= a.K) ? OOB : boff[j];
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsW, (__attribute__((address_space(3))) void *)(sb + (wave + NWV * j) * 512),
-                                                 16, off, 0, 0, 0);
+                                                 16, off, k0 * 2, 0, 0);
       }
     };
 
@@ -279,70 +328,80 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
 
     const int kt0 = sp * per_split;
     const int nk = max(0, min(nk_all, kt0 + per_split) - kt0);
-    constexpr int PW = NB - 1;     // W slices in flight ahead of the one multiplied
-    // prologue: A slice 0, W slices 0 .. PW-1
-    if (nk > 0) {
-      issueA(kt0, 0);
-      issueW(kt0, 0);
+    constexpr int PA = NA - 1, PW = NB - 1;   // slices in flight ahead of the one multiplied
+    constexpr int PMAX = PA > PW ? PA : PW;
+    static_assert(PMAX * (AJ + BJ) <= 63, "outstanding loads within the vmcnt range");
+    // prologue: A[0 .. PA-1] and W[0 .. PW-1], interleaved by slice
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j) {
+      if (j < PA && j < nk) issueA(kt0 + j, j % NA);
+      if (j < PW && j < nk) issueW(kt0 + j, j % NB);
     }
+    // One 16-k sub-step: the WM x WN MFMAs on the fragments in (fa, fb), each
+    // fragment register refilled with sub-step nks of the slice at (na, nb)
+    // right after its last use (A fragment i after MFMA (i, WN-1), W fragment
+    // j after MFMA (WM-1, j)), so one set of fragment registers serves the
+    // pipeline; nks < 0 refills nothing.
+    auto substep = [&](bf16x8 (&fa)[WM], bf16x8 (&fb)[WN], const uint16_t *na, const uint16_t *nb, int nks) {
+      const int kc = 2 * nks + kh;
 #pragma unroll
-    for (int p = 1; p < PW; ++p)
-      if (p < nk) issueW(kt0 + p, p);
-    for (int it = 0; it < nk; ++it) {
-      // issue order: A[0] W[0] .. W[PW-1], then per iteration A[it+1] W[it+PW].
-      // A[it] and W[it] are done once at most the W slices issued after A[it]
-      // remain: W[1 .. PW-1] at it = 0, W[it+PW-1] later (when they exist)
-      if constexpr (PW == 2) {
-        if (it + 1 < nk) wait_vm<BJ>();
-        else wait_vm<0>();
-      } else {                     // PW == 3
-        if (it == 0) {
-          if (nk > 2) wait_vm<2 * BJ>();
-          else if (nk == 2) wait_vm<BJ>();
-          else wait_vm<0>();
-        } else if (it + 2 < nk) {
-          wait_vm<BJ>();
-        } else {
-          wait_vm<0>();
-        }
-      }
-      ring_barrier();
-      const uint16_t *sa = ldsA + (it % NA) * (TM * TK);
-      const uint16_t *sb = ldsW + (it % NB) * (TN * TK);
-      bf16x8 fa[2][WM], fb[2][WN];
-      // first 16-k fragments, then the next stages' loads while they are in flight
+      for (int i = 0; i < WM; ++i) {
 #pragma unroll
-      for (int i = 0; i < WM; ++i) fa[0][i] = *(const bf16x8 *)(sa + afrag[i] + 8 * (kh ^ arx[i]));
-#pragma unroll
-      for (int j = 0; j < WN; ++j) fb[0][j] = *(const bf16x8 *)(sb + bfrag[j] + 8 * (kh ^ brx[j]));
-      if (it + 1 < nk) issueA(kt0 + it + 1, (it + 1) % NA);
-      if (it + PW < nk) issueW(kt0 + it + PW, (it + PW) % NB);
-#pragma unroll
-      for (int ks = 0; ks < TK / 16; ++ks) {
-        const int cur = ks & 1;
-        if (ks + 1 < TK / 16) {
-          const int kc = 2 * (ks + 1) + kh;
-#pragma unroll
-          for (int i = 0; i < WM; ++i) fa[cur ^ 1][i] = *(const bf16x8 *)(sa + afrag[i] + 8 * (kc ^ arx[i]));
-#pragma unroll
-          for (int j = 0; j < WN; ++j) fb[cur ^ 1][j] = *(const bf16x8 *)(sb + bfrag[j] + 8 * (kc ^ brx[j]));
-        }
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-          for (int j = 0; j < WN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
-        // interleave: the next step's fragment reads between this step's MFMAs
-        if (ks + 1 < TK / 16) {
-          constexpr int NR = WM + WN, NMF = WM * WN, NI = NR < NMF ? NR : NMF;
-#pragma unroll
-          for (int q = 0; q < NI; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        for (int j = 0; j < WN; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (nks >= 0 && i == WM - 1) {
+            fb[j] = *(const bf16x8 *)(nb + bfrag[j] + 8 * (kc ^ brx[j]));
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          if (NMF > NI) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NI, 0);
-          if (NR > NI) __builtin_amdgcn_sched_group_barrier(0x100, NR - NI, 0);
         }
+        if (nks >= 0) {
+          fa[i] = *(const bf16x8 *)(na + afrag[i] + 8 * (kc ^ arx[i]));
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      }
+    };
+    auto first_frags = [&](const uint16_t *sa, const uint16_t *sb, bf16x8 (&fa)[WM], bf16x8 (&fb)[WN]) {
+#pragma unroll
+      for (int i = 0; i < WM; ++i) fa[i] = *(const bf16x8 *)(sa + afrag[i] + 8 * (kh ^ arx[i]));
+#pragma unroll
+      for (int j = 0; j < WN; ++j) fb[j] = *(const bf16x8 *)(sb + bfrag[j] + 8 * (kh ^ brx[j]));
+    };
+    bf16x8 fa[WM], fb[WN];
+    if (T::SKEW && wave >= NWV / 2) {
+      // The second half of the waves runs one 16-k sub-step behind the first:
+      // at each barrier it holds the last sub-step of the previous slice in
+      // registers, so on every SIMD one wave has MFMAs ready while the other
+      // waits for its first fragments.  Each accumulator still takes the k
+      // sub-steps in order.
+      for (int it = 0; it < nk; ++it) {
+        wait_vm_le<0, PMAX * (AJ + BJ)>(loads_after<PA, PW, AJ, BJ>(it, nk));
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the previous slice is out of LDS
+        ring_barrier();
+        const uint16_t *sa = ldsA + (it % NA) * (TM * TK);
+        const uint16_t *sb = ldsW + (it % NB) * (TN * TK);
+        if (it == 0) first_frags(sa, sb, fa, fb);
+        else substep(fa, fb, sa, sb, 0);            // last sub-step of the previous slice
+        if (it + PA < nk) issueA(kt0 + it + PA, (it + PA) % NA);
+        if (it + PW < nk) issueW(kt0 + it + PW, (it + PW) % NB);
+#pragma unroll
+        for (int ks = 0; ks < TK / 16 - 1; ++ks) substep(fa, fb, sa, sb, ks + 1);
+      }
+      if (nk > 0) substep(fa, fb, nullptr, nullptr, -1);
+    } else {
+      for (int it = 0; it < nk; ++it) {
+        // this wave's loads of A[it] and W[it] are done once at most the loads
+        // issued after them remain
+        wait_vm_le<0, PMAX * (AJ + BJ)>(loads_after<PA, PW, AJ, BJ>(it, nk));
+        ring_barrier();
+        const uint16_t *sa = ldsA + (it % NA) * (TM * TK);
+        const uint16_t *sb = ldsW + (it % NB) * (TN * TK);
+        // first 16-k fragments, then the next slices' loads while they are in flight
+        first_frags(sa, sb, fa, fb);
+        if (it + PA < nk) issueA(kt0 + it + PA, (it + PA) % NA);
+        if (it + PW < nk) issueW(kt0 + it + PW, (it + PW) % NB);
+#pragma unroll
+        for (int ks = 0; ks < TK / 16; ++ks) substep(fa, fb, sa, sb, ks + 1 < TK / 16 ? ks + 1 : -1);
       }
     }
     // every wave is done with the rings before the next task's prologue refills them
@@ -687,6 +746,8 @@ int launch_epi(int kid, const GemmArgs &a, hipStream_t s) {
       return DCUT_EINVAL;
     const int g = (cu_count() + 7) / 8 * 8;
     return launch(kid, k_gemm_dual<EPI>, dim3((unsigned)g), dim3(Big::THREADS), Big::LDS, s, a);
+  } else if constexpr (EPI == EPI_SAMPLE) {
+    return launch_tile<EPI, BigFlat>(kid, a, s);
   } else {
     return launch_tile<EPI, Big>(kid, a, s);
   }
