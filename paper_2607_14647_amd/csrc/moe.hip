@@ -7,7 +7,7 @@
 // renormalised over the chosen experts.
 //
 // Determinism and causality: a row's routing, its expert GEMM rows and its
-// combine depend only on that row.  Grouping sorts the unique keys
+// combine depend only on that row.  Grouping orders the assignments by
 // (expert, row * top_k + slot), so each expert's rows appear in row order,
 // and the combine adds the top_k expert outputs of a row in slot order.
 #include "dcut_internal.h"
@@ -104,68 +104,80 @@ k_moe_route(const float *__restrict__ logits, int E, int k, int M_max, const int
   }
 }
 
-// One workgroup: sort the K* * k keys (expert << 20 | row * k + slot), then the
-// gather rows, inverse positions and the (expert, first, end) row tiles.
+// One workgroup: a stable counting sort of the K* * k assignments j = row * k +
+// slot by expert (each expert's assignments in increasing j, the order of the
+// keys (expert, j)), then the gather rows, inverse positions and the (expert,
+// first, end) row tiles.  Assignments go in chunks of one per thread; within a
+// wave, the lanes holding the same expert are found with one ballot per bit of
+// the expert id, and the per-wave counts of the chunk place each assignment
+// after those of earlier waves and earlier chunks.
 __global__ void __launch_bounds__(1024)
 k_moe_group(const int32_t *__restrict__ ids, int E, int k, int M_max, const int32_t *__restrict__ m_count,
             int32_t *__restrict__ row_of, int32_t *__restrict__ inv, int32_t *__restrict__ tiles,
             int32_t *__restrict__ n_tiles) {
-  extern __shared__ uint32_t keys[];
-  __shared__ int s_cnt[256];
+  __shared__ int s_base[256];           // per expert: count, then the next free position
+  __shared__ int s_wcnt[16][256];       // per wave and expert: assignments of the current chunk
   __shared__ int s_wave[17];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = blockDim.x >> 6;
   const int N = min(*m_count, M_max) * k;
-  int NP = 64;
-  while (NP < N) NP <<= 1;
-  for (int j = tid; j < NP; j += blockDim.x) {
-    uint32_t key = 0xffffffffu;
-    if (j < N) {
-      int e = ids[j];
-      e = e < 0 ? 0 : (e >= E ? E - 1 : e);
-      key = ((uint32_t)e << 20) | (uint32_t)j;
-    }
-    keys[j] = key;
-  }
-  for (int e = tid; e < 256; e += blockDim.x) s_cnt[e] = 0;
-  for (int size = 2; size <= NP; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      __syncthreads();
-      for (int q = tid; q < (NP >> 1); q += blockDim.x) {
-        int lo = 2 * q - (q & (stride - 1));
-        int hi = lo + stride;
-        uint32_t x = keys[lo], y = keys[hi];
-        bool asc = (lo & size) == 0;
-        if (asc ? (x > y) : (x < y)) {
-          keys[lo] = y;
-          keys[hi] = x;
-        }
-      }
-    }
-  }
+  auto expert_of = [&](int j) {
+    const int e = ids[j];
+    return e < 0 ? 0 : (e >= E ? E - 1 : e);
+  };
+  for (int e = tid; e < 256; e += blockDim.x) s_base[e] = 0;
+  for (int i = tid; i < 16 * 256; i += blockDim.x) (&s_wcnt[0][0])[i] = 0;
   __syncthreads();
-  for (int p = tid; p < N; p += blockDim.x) {
-    uint32_t key = keys[p];
-    int a = (int)(key & 0xfffffu);
-    row_of[p] = a / k;
-    inv[a] = p;
-    atomicAdd(&s_cnt[key >> 20], 1);
-  }
+  for (int j = tid; j < N; j += blockDim.x) atomicAdd(&s_base[expert_of(j)], 1);
   __syncthreads();
   // exclusive scans over experts: row offsets and tile offsets
-  int cnt = tid < E ? s_cnt[tid] : 0;
-  int ntl = (cnt + TILE_M - 1) / TILE_M;
+  const int cnt = tid < E ? s_base[tid] : 0;
+  const int ntl = (cnt + TILE_M - 1) / TILE_M;
   int tot_r, tot_t;
-  int off_r = block_exclusive_scan(cnt, s_wave, &tot_r);
-  int off_t = block_exclusive_scan(ntl, s_wave, &tot_t);
+  const int off_r = block_exclusive_scan(cnt, s_wave, &tot_r);
+  const int off_t = block_exclusive_scan(ntl, s_wave, &tot_t);
   if (tid < E) {
-    for (int j = 0; j < ntl; ++j) {
-      int tt = off_t + j;
+    for (int q = 0; q < ntl; ++q) {
+      const int tt = off_t + q;
       tiles[3 * tt] = tid;
-      tiles[3 * tt + 1] = off_r + j * TILE_M;
+      tiles[3 * tt + 1] = off_r + q * TILE_M;
       tiles[3 * tt + 2] = off_r + cnt;
     }
+    s_base[tid] = off_r;
   }
   if (tid == 0) n_tiles[0] = tot_t;
+  __syncthreads();
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int c0 = 0; c0 < N; c0 += blockDim.x) {
+    const int j = c0 + tid;
+    const bool live = j < N;
+    const int e = live ? expert_of(j) : 0;
+    unsigned long long same = __ballot(live);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (e >> b) & 1;
+      const unsigned long long m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    const int wrank = __popcll(same & below);
+    if (live && wrank == 0) s_wcnt[wv][e] = __popcll(same);
+    __syncthreads();
+    if (live) {
+      int p = s_base[e] + wrank;
+      for (int v = 0; v < wv; ++v) p += s_wcnt[v][e];
+      row_of[p] = j / k;
+      inv[j] = p;
+    }
+    __syncthreads();
+    for (int e2 = tid; e2 < E; e2 += blockDim.x) {
+      int add = 0;
+      for (int v = 0; v < nw; ++v) {
+        add += s_wcnt[v][e2];
+        s_wcnt[v][e2] = 0;
+      }
+      s_base[e2] += add;
+    }
+    __syncthreads();
+  }
 }
 
 // One workgroup per row: out[t] += sum_s w[t][s] * eo[inv[t*k + s]], slot order.
@@ -221,9 +233,7 @@ int moe_launch(const MoeArgs &m, hipStream_t s) {
   DCUT_TRY(gemm_launch(DCUT_KERNEL_MOE, EPI_STORE_F32, r, s));
   DCUT_TRY(launch(DCUT_KERNEL_MOE, k_moe_route, dim3((M + 3) / 4), dim3(256), 0, s, (const float *)logits,
                   m.E, m.top_k, M, m.m_count, ids, wts));
-  int NP = 64;
-  while (NP < A) NP <<= 1;
-  DCUT_TRY(launch(DCUT_KERNEL_MOE, k_moe_group, dim3(1), dim3(1024), (size_t)NP * 4, s, (const int32_t *)ids,
+  DCUT_TRY(launch(DCUT_KERNEL_MOE, k_moe_group, dim3(1), dim3(1024), 0, s, (const int32_t *)ids,
                   m.E, m.top_k, M, m.m_count, row_of, inv, tiles, ntiles));
   // gathered rows of h through the grouped gate-up GEMM with the SwiGLU epilogue
   GemmArgs gu = {};
