@@ -17,10 +17,11 @@
 // Scheduling: the grid is persistent (at most one wave of workgroups); every
 // workgroup reads the live row count M (K*) on the device and walks only the
 // tiles that exist, so rows beyond K* cost nothing.  Tasks (row tile, column
-// tile, k split) are numbered with the row tile fastest and cut into eight
-// contiguous ranges, one per XCD (the hardware deals workgroups round-robin
-// over the eight XCDs), so row tiles sharing a W slice run at the same time on
-// the same L2.
+// tile, k split) are numbered with the row tile fastest and the split slowest
+// and cut into eight contiguous ranges, one per XCD (the hardware deals
+// workgroups round-robin over the eight XCDs): row tiles sharing a W slice run
+// at the same time on the same L2, and an XCD reads the A columns of one or
+// two splits only, not all of A.
 //
 // Determinism and causality: every output element is the same sequence of
 // MFMA k-steps from k = 0 upwards whatever the tile shape; split-K partials are
@@ -206,7 +207,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
   const int l32 = lane & 31, kh = lane >> 5;
   const int lr = lane / CPR, lc = lane % CPR;
 
-  // live tasks: (row tile, split, column tile), row tile fastest
+  // live tasks: (row tile, column tile, split), row tile fastest, split slowest
   const int M = min(*a.m_count, a.M_max);
   const int nMT = a.tiles ? *a.n_tiles : (M + TM - 1) / TM;
   const int nNT = n_col_tiles<EPI>(a, TN);
@@ -247,7 +248,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
   for (int task = lo + (int)(blockIdx.x >> 3); task < hi; task += per_xcd) {
     const int mt = task % nMT;
     const int rest = task / nMT;
-    const int sp = rest % splits, nt = rest / splits;
+    const int nt = rest % nNT, sp = rest / nNT;
     int m0 = mt * TM, Mlim = M;
     const uint16_t *Wb = a.W;
     if (a.tiles) {

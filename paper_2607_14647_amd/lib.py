@@ -139,7 +139,8 @@ def workspace_bytes(which: int, cfg: Optional[LayerCfg], B: int, D: int) -> int:
 
 
 def profile_arm(kernel: str, start=None, stop=None) -> None:
-    """Arm the timing hook for one kernel on this thread (torch.cuda.Event pair, already recorded once)."""
+    """Arm the timing hook for one kernel on this thread: `start` and `stop` carry a HIP event handle in
+    `cuda_event` (a torch.cuda.Event already recorded once, or an event created directly)."""
     kid = KERNELS[kernel]
     s = C.c_void_p(start.cuda_event) if start is not None else None
     e = C.c_void_p(stop.cuda_event) if stop is not None else None
