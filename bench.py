@@ -397,6 +397,35 @@ def main():
             out[nm] = round(1000.0 * statistics.mean(a.elapsed_time(b) for a, b in pairs), 2)
         return out
 
+    def stream_ceiling():
+        """The HBM -> LDS stream rate of the library's stream probe (the load path of the GEMM
+        and attention kernels) over a 1 GiB buffer: with two workgroups per CU (the attainable
+        rate the HBM-bound kernels are compared with) and with 32 workgroups (one CU's share)."""
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        buf.fill_(1)
+
+        def rate(views, wg, warm):
+            """GB/s over the views, one probe each, after an untimed probe of `warm`"""
+            L.stream_probe(warm, wg)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for v in views:
+                L.stream_probe(v, wg)
+            b.record(stream)
+            torch.cuda.synchronize()
+            return sum(v.numel() for v in views) / (a.elapsed_time(b) * 1e-3) / 1e9
+
+        full = rate([buf] * 5, 2 * cus, buf)     # 1 GiB a pass: four times the 256 MB MALL
+        # one CU's share: 32 workgroups, each pass over a 128 MB range not read since the full passes
+        sl = 32 * 4 * (1 << 20)
+        one = rate([buf[r * sl:(r + 1) * sl] for r in range(5)], 32, buf[5 * sl:6 * sl])
+        del buf
+        log(f"stream probe: {full:.0f} GB/s with {2 * cus} workgroups; {one / 32:.1f} GB/s per CU (32 workgroups)")
+        return dict(stream_gbps=round(full, 1), unit="GB/s", workgroups=2 * cus, bytes=1 << 30,
+                    per_cu_gbps=round(one / 32, 2), peak=PEAK_HBM_GBS, frac_of_peak=round(full / PEAK_HBM_GBS, 4),
+                    kernel="dcut_stream_probe: buffer loads into LDS, 16 B per lane, 8 KB in flight per wave")
+
     def timed_region(fn, dominant):
         """`--steps` steps after `--warmup`, bracketed by synchronisations; the dominant kernel of
         every step timed by events on the launch stream (the library's hook)."""
@@ -596,6 +625,13 @@ def main():
     rl["avg_us"] = round(dom_us, 2)
     fractions = {k: kernel_fraction(k, cfg, Kstar, st["ctx_len"], v) for k, v in breakdown.items()}
     fractions = {k: v for k, v in fractions.items() if v is not None}
+    attainable = stream_ceiling()
+    if rl["bound"] == "hbm":
+        rl["frac_of_attainable"] = round(rl["achieved"] / attainable["stream_gbps"], 4)
+    for k, f in fractions.items():
+        fl, by = kernel_work(k, cfg, Kstar, st["ctx_len"])
+        if f["bound"] == "hbm":
+            f["frac_of_attainable"] = round(by / (f["us"] * 1e-6) / 1e9 / attainable["stream_gbps"], 4)
     counted = counted_step_bytes(workload, Kstar, args.layers) if args.temperature == 0 else None
     fixed = {}
     for rho, m in (("0.25", 4), ("0.50", 8), ("0.75", 12), ("1.00", 16)):
@@ -629,6 +665,7 @@ def main():
         hbm_counted=None if counted is None else dict(
             gbps=round(counted[0] / (ms_per_step * 1e-3) / 1e9, 1), bytes=int(counted[0]), kernels=counted[1]),
         roofline=rl,
+        attainable=attainable,
         kernel_us=breakdown,
         kernel_roofline=fractions,
         unpruned=unpruned,

@@ -405,6 +405,20 @@ enum {
 };
 int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop);
 
+/* Measurement aid (not a step of the method): streams `bytes` from the dev
+ * buffer `src` into LDS the way the GEMM and attention kernels load their
+ * operands (buffer loads with the LDS destination, 16 bytes per lane, eight
+ * 1 KB loads in flight per wave), and writes nothing.  `workgroups` workgroups
+ * of four waves split the buffer into equal contiguous ranges, one per wave.
+ * Timing the call on `stream` gives the HBM stream rate attainable through
+ * this load path (with at least one workgroup per CU) or one CU's share (with
+ * fewer workgroups than CUs); bench.py reports it beside the roofline.
+ * Requirements: src 16-byte aligned, 1 <= workgroups <= 65536, bytes a
+ * non-zero multiple of workgroups * 4 KB (DCUT_EINVAL otherwise), and at most
+ * 2 GiB - 1 KB per wave (DCUT_EUNSUPPORTED otherwise).  The buffer is read
+ * only and stays owned by the caller. */
+int dcut_stream_probe(const void *src, size_t bytes, int workgroups, hipStream_t stream);
+
 #pragma GCC visibility pop
 #ifdef __cplusplus
 }

@@ -539,7 +539,7 @@ __device__ __forceinline__ void gemm_tasks(const GemmArgs &a) {
             const uint32_t c = (uint32_t)(col0 + 32 * j);
             float v = acc[i][j][r];
             if constexpr (EPI == EPI_SAMPLE) v = v * a.inv_temp + noise[j];
-            const uint32_t o = c < (uint32_t)a.N ? orderable(v) : 0u;
+            const uint32_t o = c < (uint32_t)a.N ? order_key(v) : 0u;
             const bool up = o > bo;
             bo = up ? o : bo;
             bc = up ? c : bc;

@@ -13,6 +13,13 @@ __device__ __forceinline__ uint32_t orderable(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// The same key without a select: the sign smeared by an arithmetic shift,
+// with the top bit set, flips the magnitude bits of negative values only.
+__device__ __forceinline__ uint32_t order_key(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
+}
+
 // Philox4x32 with ten rounds (Salmon, Moraes, Dror, Shaw, SC 2011): each round
 // multiplies words 0 and 2 by the two Philox constants and mixes the high and
 // low halves with words 1 and 3 and the key; the key advances by the two Weyl

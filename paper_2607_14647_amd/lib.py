@@ -26,7 +26,7 @@ RS_SCAN, RS_FIXED, RS_HISTORY = 0, 1, 2
 EXPORTS = ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_argmax_static",
            "dcut_lm_head_static_scratch_bytes", "dcut_accept", "dcut_lm_head_sample", "dcut_select_rs",
            "dcut_accept_rs", "dcut_workspace_bytes", "dcut_strerror", "dcut_budgets_from_ratios",
-           "dcut_nearest_batch", "dcut_profile_arm"]
+           "dcut_nearest_batch", "dcut_profile_arm", "dcut_stream_probe"]
 
 
 class DcutError(RuntimeError):
@@ -79,6 +79,7 @@ def _load() -> C.CDLL:
     lib.dcut_budgets_from_ratios.argtypes = [i32, i32, i32, vp, vp, vp]
     lib.dcut_nearest_batch.argtypes = [i32, i32, vp]
     lib.dcut_profile_arm.argtypes = [i32, vp, vp]
+    lib.dcut_stream_probe.argtypes = [vp, sz, i32, vp]
     for f in ["dcut_select", "dcut_verify_layer", "dcut_lm_head_argmax", "dcut_lm_head_argmax_static",
               "dcut_lm_head_sample", "dcut_accept",
               "dcut_select_rs", "dcut_accept_rs", "dcut_budgets_from_ratios", "dcut_nearest_batch",
@@ -145,6 +146,13 @@ def profile_arm(kernel: str, start=None, stop=None) -> None:
     s = C.c_void_p(start.cuda_event) if start is not None else None
     e = C.c_void_p(stop.cuda_event) if stop is not None else None
     _check(_lib.dcut_profile_arm(kid, s, e), "dcut_profile_arm")
+
+
+def stream_probe(src: torch.Tensor, workgroups: int, stream=None) -> None:
+    """Stream the whole of `src` (a contiguous device tensor) through LDS with
+    `workgroups` workgroups of four waves: a measurement aid, not a step."""
+    st = _lib.dcut_stream_probe(_p(src), src.numel() * src.element_size(), int(workgroups), _stream(stream))
+    _check(st, "dcut_stream_probe")
 
 
 # ------------------------------------------------------------------ the calls

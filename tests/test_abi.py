@@ -162,6 +162,16 @@ def test_other_entry_points_reject_invalid_args():
     assert lib.dcut_profile_arm(L.KERNELS["LM_HEAD"], None, None) == L.EINVAL
     assert lib.dcut_profile_arm(0, None, None) == L.OK
     assert L.strerror(L.EHIP).startswith("HIP")
+    # stream probe: alignment, workgroup count, a size that does not split into whole 1 KB loads
+    # per wave, and a per-wave range past what one buffer resource addresses
+    sp = lib.dcut_stream_probe
+    assert sp(None, 1 << 20, 4, None) == L.EINVAL
+    assert sp(C.c_void_p(0x1008), 1 << 20, 4, None) == L.EINVAL
+    assert sp(fake, 1 << 20, 0, None) == L.EINVAL
+    assert sp(fake, 1 << 20, 65537, None) == L.EINVAL
+    assert sp(fake, 0, 4, None) == L.EINVAL
+    assert sp(fake, (1 << 20) + 1024, 4, None) == L.EINVAL
+    assert sp(fake, 4 << 31, 1, None) == L.EUNSUPPORTED
 
 
 def test_operands_past_32bit_offsets_are_rejected_before_any_launch():
