@@ -625,12 +625,13 @@ def main():
     rl["avg_us"] = round(dom_us, 2)
     fractions = {k: kernel_fraction(k, cfg, Kstar, st["ctx_len"], v) for k, v in breakdown.items()}
     fractions = {k: v for k, v in fractions.items() if v is not None}
-    attainable = stream_ceiling()
-    if rl["bound"] == "hbm":
+    # the attainable stream rate (skipped in a profiler replay of saved state, which times the step only)
+    attainable = stream_ceiling() if state is None else None
+    if attainable is not None and rl["bound"] == "hbm":
         rl["frac_of_attainable"] = round(rl["achieved"] / attainable["stream_gbps"], 4)
     for k, f in fractions.items():
         fl, by = kernel_work(k, cfg, Kstar, st["ctx_len"])
-        if f["bound"] == "hbm":
+        if attainable is not None and f["bound"] == "hbm":
             f["frac_of_attainable"] = round(by / (f["us"] * 1e-6) / 1e9 / attainable["stream_gbps"], 4)
     counted = counted_step_bytes(workload, Kstar, args.layers) if args.temperature == 0 else None
     fixed = {}
