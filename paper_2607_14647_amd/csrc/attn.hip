@@ -335,6 +335,41 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
   // the loads of up to CG chunks are issued together (one memory latency per
   // group rather than per chunk); the sums still run in chunk order
   constexpr int CG = 8;
+  constexpr int PER = HD / 64;
+  const float *pl = pp + lane * PER;
+  uint16_t *op = a.out + ((size_t)t * a.n_q + head) * HD;
+  if (nc <= CG) {
+    // every chunk's (max, sum, partial) in one memory round trip; the same
+    // operations in the same order as the two-pass loop below
+    float mv[CG], lv[CG], xv[CG][PER];
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+      mv[c] = c < nc ? pp[c * (HD + 2) + HD] : -__builtin_inff();
+      lv[c] = c < nc ? pp[c * (HD + 2) + HD + 1] : 0.0f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) xv[c][e] = c < nc ? pl[c * (HD + 2) + e] : 0.0f;
+    }
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int c = 0; c < CG; ++c) mx = fmaxf(mx, mv[c]);
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
+    float lsum = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+      if (c < nc) {
+        const float sc = (mv[c] == -__builtin_inff()) ? 0.0f : exp2f(mv[c] - mx);
+        lsum += lv[c] * sc;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] += xv[c][e] * sc;
+      }
+    }
+    const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) op[lane * PER + e] = f2bf(acc[e] * inv);
+    return;
+  }
   float mx = -__builtin_inff();
   for (int c0 = 0; c0 < nc; c0 += CG) {
     float mv[CG];
@@ -343,7 +378,6 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
 #pragma unroll
     for (int c = 0; c < CG; ++c) mx = fmaxf(mx, mv[c]);
   }
-  constexpr int PER = HD / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
@@ -371,7 +405,6 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
     }
   }
   const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
-  uint16_t *op = a.out + ((size_t)t * a.n_q + head) * HD;
 #pragma unroll
   for (int e = 0; e < PER; ++e) op[lane * PER + e] = f2bf(acc[e] * inv);
 }

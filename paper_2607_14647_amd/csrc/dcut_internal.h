@@ -28,6 +28,12 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
   return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
 }
 
+// RoPE (rotate-half) of the pair (x1, x2) = dimensions (j, j + hd/2) of one row,
+// cs = (cos, sin) of the row's position and frequency j.
+__device__ __forceinline__ float2 rope_pair(float x1, float x2, float2 cs) {
+  return make_float2(x1 * cs.x - x2 * cs.y, x2 * cs.x + x1 * cs.y);
+}
+
 // Split-K partial sums in split order, with the loads of four splits issued
 // together (one memory round trip per four splits).  load(s) returns split s;
 // indices past the last split re-read it, and the adds are selects rather than

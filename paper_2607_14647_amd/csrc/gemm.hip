@@ -169,9 +169,9 @@ __device__ __forceinline__ void qkv_emit(const GemmArgs &a, int gm, int head, in
   const int hd = a.head_dim, half = hd >> 1;
   float o1 = x1, o2 = x2;
   if (head < a.n_q + a.n_kv) {
-    const float2 cs = a.rope_cs[(size_t)gm * half + j];
-    o1 = x1 * cs.x - x2 * cs.y;
-    o2 = x2 * cs.x + x1 * cs.y;
+    const float2 r = rope_pair(x1, x2, a.rope_cs[(size_t)gm * half + j]);
+    o1 = r.x;
+    o2 = r.y;
   }
   if (head < a.n_q) {
     uint16_t *q = a.out_bf16 + (size_t)gm * a.ldo + head * hd;
@@ -666,22 +666,54 @@ k_splitk_reduce(const float *__restrict__ part, int splits, int M_max, int N,
   *o = acc;
 }
 
-// QKV split-K epilogue: one thread per (row, head, RoPE pair); the partials of
-// dimensions j and j + hd/2 added in split order, then the QKV epilogue.
+// QKV split-K epilogue: one thread per (row, head, four consecutive RoPE pairs);
+// the partials of dimensions j..j+3 and j+hd/2..j+hd/2+3 added in split order,
+// then the QKV epilogue on each pair (the element-wise operations of qkv_emit),
+// stored four bf16 at a time.
 __global__ void __launch_bounds__(256)
 k_qkv_reduce(GemmArgs a) {
   const int m = blockIdx.y;
   if (m >= *a.m_count) return;
-  const int half = a.head_dim >> 1, nh = a.n_q + 2 * a.n_kv;
+  const int hd = a.head_dim, half = hd >> 1, nh = a.n_q + 2 * a.n_kv;
   const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= nh * half) return;
-  const int head = idx / half, j = idx - head * half;
-  const size_t c1 = (size_t)head * a.head_dim + j, c2 = c1 + half;
-  const float2 x = sum_splits<float2>(a.splits, [&](int s) {
+  if (idx >= nh * (half / 4)) return;
+  const int head = idx / (half / 4), j = 4 * (idx - head * (half / 4));
+  const size_t c1 = (size_t)head * hd + j, c2 = c1 + half;
+  const f4x2 x = sum_splits<f4x2>(a.splits, [&](int s) {
     const float *q = a.split_part + ((size_t)s * a.M_max + m) * a.N;
-    return make_float2(q[c1], q[c2]);
+    return f4x2{*(const float4 *)(q + c1), *(const float4 *)(q + c2)};
   });
-  qkv_emit(a, m, head, j, x.x, x.y);
+  float o1[4] = {x.a.x, x.a.y, x.a.z, x.a.w}, o2[4] = {x.b.x, x.b.y, x.b.z, x.b.w};
+  if (head < a.n_q + a.n_kv) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float2 r = rope_pair(o1[e], o2[e], a.rope_cs[(size_t)m * half + j + e]);
+      o1[e] = r.x;
+      o2[e] = r.y;
+    }
+  }
+  uint16_t *dst;
+  if (head < a.n_q) {
+    dst = a.out_bf16 + (size_t)m * a.ldo + head * hd;
+  } else {
+    const int req = a.packed_req[m];
+    if ((unsigned)req >= (unsigned)a.n_req) return;   // not a row of this batch
+    const int slot = a.packed_pos[m];
+    const int cap = a.kv_cap[req];
+    if (slot < 0 || slot >= cap) return;
+    const int g = (head < a.n_q + a.n_kv) ? head - a.n_q : head - a.n_q - a.n_kv;
+    dst = (head < a.n_q + a.n_kv ? a.kv_k : a.kv_v) + a.kv_base[req] + ((size_t)g * cap + slot) * hd;
+  }
+  if (((uintptr_t)(dst + j) & 7) == 0) {
+    *(uint2 *)(dst + j) = make_uint2(pack_bf2(o1[0], o1[1]), pack_bf2(o1[2], o1[3]));
+    *(uint2 *)(dst + j + half) = make_uint2(pack_bf2(o2[0], o2[1]), pack_bf2(o2[2], o2[3]));
+  } else {   // a cache slab base that is not a multiple of four elements
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      dst[j + e] = f2bf(o1[e]);
+      dst[j + half + e] = f2bf(o2[e]);
+    }
+  }
 }
 
 // Compute units of the current device, cached per device (atomic: calls from
@@ -719,8 +751,8 @@ int launch_tile(int kid, const GemmArgs &a, hipStream_t s) {
   DCUT_TRY(launch(kid, k_gemm<EPI, T>, dim3((unsigned)g), dim3(T::THREADS), T::LDS, s, a));
   if (splits > 1 && a.defer_reduce) return DCUT_OK;
   if (splits > 1 && EPI == EPI_QKV_ROPE) {
-    const int pairs = (a.n_q + 2 * a.n_kv) * (a.head_dim / 2);
-    return launch(DCUT_KERNEL_NONE, k_qkv_reduce, dim3((pairs + 255) / 256, a.M_max), dim3(256), 0, s, a);
+    const int quads = (a.n_q + 2 * a.n_kv) * (a.head_dim / 8);
+    return launch(DCUT_KERNEL_NONE, k_qkv_reduce, dim3((quads + 255) / 256, a.M_max), dim3(256), 0, s, a);
   }
   if (splits > 1)
     return launch(DCUT_KERNEL_NONE, k_splitk_reduce, dim3((a.N + 1023) / 1024, a.M_max), dim3(256), 0, s,

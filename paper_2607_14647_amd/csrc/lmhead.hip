@@ -52,12 +52,21 @@ k_argmax_final(const unsigned long long *__restrict__ keys, const float2 *__rest
   const unsigned long long *row = keys + (size_t)t * stride;
   unsigned long long k = 0ull;
   float m = -__builtin_inff(), sum = 0.0f;
-  for (int s = tid; s < slots; s += 256) {
-    const unsigned long long v = row[s];
-    k = v > k ? v : k;
-    if (lse) {
-      const float2 p = part[(size_t)t * stride + s];
-      lse_merge(m, sum, p.x, p.y);
+  // four slots per thread per memory round trip (one round trip for up to 1024
+  // slots), merged in the order s = tid, tid + 256, ...
+  for (int s0 = tid; s0 < slots; s0 += 1024) {
+    unsigned long long v[4];
+    float2 p[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int s = s0 + 256 * u;
+      v[u] = s < slots ? row[s] : 0ull;
+      if (lse) p[u] = s < slots ? part[(size_t)t * stride + s] : make_float2(0.0f, 0.0f);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      k = v[u] > k ? v[u] : k;
+      if (lse && s0 + 256 * u < slots) lse_merge(m, sum, p[u].x, p[u].y);
     }
   }
 #pragma unroll

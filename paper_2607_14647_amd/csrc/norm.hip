@@ -50,54 +50,106 @@ k_rmsnorm(const float *__restrict__ x_in, const uint16_t *__restrict__ embed,
   // each thread owns 8-element groups g = tid, tid + 256, ...
   const int ng = H / 8;
   float ss = 0.0f;
-  for (int gi = tid; gi < ng; gi += 256) {
-    float v[8];
-    if (xr) {
-      float4 a = *(const float4 *)(xr + gi * 8);
-      float4 b = *(const float4 *)(xr + gi * 8 + 4);
-      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-      v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-    } else {
-      uint4 u = *(const uint4 *)(er + gi * 8);
-      const uint16_t *e = (const uint16_t *)&u;
+  if (ng <= 4 * 256) {
+    // the row in registers: every load issued at once, the row read once, and the
+    // same sum of squares (groups ascending, elements ascending) as the loop below
+    float v[4][8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = bf2f(e[j]);
+    for (int q = 0; q < 4; ++q) {
+      const int gi = tid + 256 * q;
+      if (gi >= ng) break;
+      if (xr) {
+        const float4 a = *(const float4 *)(xr + gi * 8), b = *(const float4 *)(xr + gi * 8 + 4);
+        v[q][0] = a.x; v[q][1] = a.y; v[q][2] = a.z; v[q][3] = a.w;
+        v[q][4] = b.x; v[q][5] = b.y; v[q][6] = b.z; v[q][7] = b.w;
+      } else {
+        uint4 u = *(const uint4 *)(er + gi * 8);
+        const uint16_t *e = (const uint16_t *)&u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[q][j] = bf2f(e[j]);
+      }
     }
-    if (x_copy && x_copy != x_in) {
-      float *dst = x_copy + (size_t)t * H + gi * 8;
-      *(float4 *)dst = make_float4(v[0], v[1], v[2], v[3]);
-      *(float4 *)(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int gi = tid + 256 * q;
+      if (gi >= ng) break;
+      if (x_copy && x_copy != x_in) {
+        float *dst = x_copy + (size_t)t * H + gi * 8;
+        *(float4 *)dst = make_float4(v[q][0], v[q][1], v[q][2], v[q][3]);
+        *(float4 *)(dst + 4) = make_float4(v[q][4], v[q][5], v[q][6], v[q][7]);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss += v[q][j] * v[q][j];
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) ss += v[j] * v[j];
-  }
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+    if ((tid & 63) == 0) s_red[tid >> 6] = ss;
+    __syncthreads();
+    const float tot = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+    const float r = 1.0f / sqrtf(tot / (float)H + eps);
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
-  if ((tid & 63) == 0) s_red[tid >> 6] = ss;
-  __syncthreads();
-  const float tot = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
-  const float r = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int gi = tid; gi < ng; gi += 256) {
-    float v[8];
-    if (xr) {
-      float4 a = *(const float4 *)(xr + gi * 8);
-      float4 b = *(const float4 *)(xr + gi * 8 + 4);
-      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-      v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-    } else {
-      uint4 u = *(const uint4 *)(er + gi * 8);
-      const uint16_t *e = (const uint16_t *)&u;
+    for (int q = 0; q < 4; ++q) {
+      const int gi = tid + 256 * q;
+      if (gi >= ng) break;
+      uint4 gv = *(const uint4 *)(gain + gi * 8);
+      const uint16_t *gg = (const uint16_t *)&gv;
+      uint4 o;
+      uint32_t *ow = (uint32_t *)&o;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = bf2f(e[j]);
+      for (int j = 0; j < 4; ++j)
+        ow[j] = pack_bf2(v[q][2 * j] * r * bf2f(gg[2 * j]), v[q][2 * j + 1] * r * bf2f(gg[2 * j + 1]));
+      *(uint4 *)(h_out + (size_t)t * H + gi * 8) = o;
     }
-    uint4 gv = *(const uint4 *)(gain + gi * 8);
-    const uint16_t *gg = (const uint16_t *)&gv;
-    uint4 o;
-    uint32_t *ow = (uint32_t *)&o;
+  } else {
+    for (int gi = tid; gi < ng; gi += 256) {
+      float v[8];
+      if (xr) {
+        float4 a = *(const float4 *)(xr + gi * 8);
+        float4 b = *(const float4 *)(xr + gi * 8 + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+      } else {
+        uint4 u = *(const uint4 *)(er + gi * 8);
+        const uint16_t *e = (const uint16_t *)&u;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      ow[j] = pack_bf2(v[2 * j] * r * bf2f(gg[2 * j]), v[2 * j + 1] * r * bf2f(gg[2 * j + 1]));
-    *(uint4 *)(h_out + (size_t)t * H + gi * 8) = o;
+        for (int j = 0; j < 8; ++j) v[j] = bf2f(e[j]);
+      }
+      if (x_copy && x_copy != x_in) {
+        float *dst = x_copy + (size_t)t * H + gi * 8;
+        *(float4 *)dst = make_float4(v[0], v[1], v[2], v[3]);
+        *(float4 *)(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss += v[j] * v[j];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+    if ((tid & 63) == 0) s_red[tid >> 6] = ss;
+    __syncthreads();
+    const float tot = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+    const float r = 1.0f / sqrtf(tot / (float)H + eps);
+    for (int gi = tid; gi < ng; gi += 256) {
+      float v[8];
+      if (xr) {
+        float4 a = *(const float4 *)(xr + gi * 8);
+        float4 b = *(const float4 *)(xr + gi * 8 + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+      } else {
+        uint4 u = *(const uint4 *)(er + gi * 8);
+        const uint16_t *e = (const uint16_t *)&u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = bf2f(e[j]);
+      }
+      uint4 gv = *(const uint4 *)(gain + gi * 8);
+      const uint16_t *gg = (const uint16_t *)&gv;
+      uint4 o;
+      uint32_t *ow = (uint32_t *)&o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        ow[j] = pack_bf2(v[2 * j] * r * bf2f(gg[2 * j]), v[2 * j + 1] * r * bf2f(gg[2 * j + 1]));
+      *(uint4 *)(h_out + (size_t)t * H + gi * 8) = o;
+    }
   }
   if (rope_cs) {
     const int half = head_dim >> 1;
