@@ -183,8 +183,10 @@ k_attn(AttnArgs a) {
       const int r = q * RPI + lrow;                // key row within the tile
       const int p = p0 + r;
       const unsigned off = p < kend ? (unsigned)(p * ROWB + 16 * (lchk ^ (r % CPR))) : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (lds_void *)(st + q * 1024), 16, off, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (lds_void *)(st + TILEB + q * 1024), 16, off, 0, 0, 0);
+      // each key is read once: non-temporal loads (cache policy nt) keep the
+      // stream from displacing reused lines in L2
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rK, (lds_void *)(st + q * 1024), 16, off, 0, 0, CPOL_NT);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rV, (lds_void *)(st + TILEB + q * 1024), 16, off, 0, 0, CPOL_NT);
     }
   };
 

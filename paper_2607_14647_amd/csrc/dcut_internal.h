@@ -28,6 +28,10 @@ __device__ __forceinline__ uint32_t pack_bf2(float a, float b) {
   return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
 }
 
+// Cache-policy bits of a vector memory instruction (the last operand of the
+// buffer-load builtins): nt marks a load as streaming (non-temporal).
+constexpr int CPOL_NT = 2;
+
 // RoPE (rotate-half) of the pair (x1, x2) = dimensions (j, j + hd/2) of one row,
 // cs = (cos, sin) of the row's position and frequency j.
 __device__ __forceinline__ float2 rope_pair(float x1, float x2, float2 cs) {
