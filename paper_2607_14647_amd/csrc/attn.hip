@@ -33,7 +33,6 @@ namespace dcut {
 namespace {
 
 constexpr int KT = 32;     // keys per tile
-constexpr int NSTAGE = 4;  // LDS ring stages: three tiles in flight while one is used
 
 typedef short short4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -78,8 +77,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void *base,
   return __builtin_amdgcn_make_buffer_rsrc((void *)(((uintptr_t)hi << 32) | lo), (short)0, n, 0x00020000);
 }
 
-template <int HD, int NW>
-__global__ void __launch_bounds__(NW * 64)
+// NSTAGE LDS ring stages: NSTAGE - 1 tiles in flight while one is used.  At
+// most 168 registers (three waves per SIMD), so three 4-wave workgroups with
+// 3-stage rings (48 KB of LDS each) share a CU.
+template <int HD, int NW, int NSTAGE>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
 k_attn(AttnArgs a) {
   constexpr int ROWB = HD * 2;              // bytes per key row
   constexpr int CPR = ROWB / 16;            // 16-byte chunks per key row (8 or 16)
@@ -413,13 +415,18 @@ k_attn_combine(AttnArgs a, const int32_t *__restrict__ packed_req, int rows_max)
 
 template <int HD>
 int launch_hd(const AttnArgs &a, int rows_max, const int32_t *packed_req, int waves, hipStream_t s) {
-  // at least 8 waves: the extra waves share the tile loads, which measured
-  // faster than 4 waves per workgroup (16 waves measured slower)
+  // Up to 64 rows per item: 4 waves and a 3-stage ring, three workgroups per
+  // CU, so one streams on while another starts or finishes an item.  Up to 128
+  // or 256 rows: 8 or 16 waves and a 4-stage ring, two or one per CU (8 waves
+  // measured faster than 4 at two workgroups per CU: the extra waves share
+  // the tile loads).
   const dim3 grid(a.B * a.n_kv * a.max_chunks);
-  if (waves <= 8) {
-    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 8>, grid, dim3(512), 0, s, a));
+  if (waves <= 4) {
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 4, 3>, grid, dim3(256), 0, s, a));
+  } else if (waves <= 8) {
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 8, 4>, grid, dim3(512), 0, s, a));
   } else {
-    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 16>, grid, dim3(1024), 0, s, a));
+    DCUT_TRY(launch(DCUT_KERNEL_ATTN, k_attn<HD, 16, 4>, grid, dim3(1024), 0, s, a));
   }
   int nw = rows_max * a.n_q;
   return launch(DCUT_KERNEL_ATTN_COMBINE, k_attn_combine<HD>, dim3((nw + 3) / 4), dim3(256), 0, s, a,
