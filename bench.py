@@ -424,7 +424,7 @@ def main():
         log(f"stream probe: {full:.0f} GB/s with {2 * cus} workgroups; {one / 32:.1f} GB/s per CU (32 workgroups)")
         return dict(stream_gbps=round(full, 1), unit="GB/s", workgroups=2 * cus, bytes=1 << 30,
                     per_cu_gbps=round(one / 32, 2), peak=PEAK_HBM_GBS, frac_of_peak=round(full / PEAK_HBM_GBS, 4),
-                    kernel="dcut_stream_probe: buffer loads into LDS, 16 B per lane, 8 KB in flight per wave")
+                    kernel="dcut_stream_probe: non-temporal buffer loads into LDS, 16 B per lane, 8 KB in flight per wave")
 
     def timed_region(fn, dominant):
         """`--steps` steps after `--warmup`, bracketed by synchronisations; the dominant kernel of

@@ -408,7 +408,8 @@ int dcut_profile_arm(int kernel, hipEvent_t start, hipEvent_t stop);
 /* Measurement aid (not a step of the method): streams `bytes` from the dev
  * buffer `src` into LDS the way the GEMM and attention kernels load their
  * operands (buffer loads with the LDS destination, 16 bytes per lane, eight
- * 1 KB loads in flight per wave), and writes nothing.  `workgroups` workgroups
+ * 1 KB loads in flight per wave, non-temporal as the attention's cache
+ * stream), and writes nothing.  `workgroups` workgroups
  * of four waves split the buffer into equal contiguous ranges, one per wave.
  * Timing the call on `stream` gives the HBM stream rate attainable through
  * this load path (with at least one workgroup per CU) or one CU's share (with
