@@ -26,11 +26,13 @@
  *     buffer; the library never allocates device memory.  Scratch memory comes
  *     from the caller through (ws, ws_bytes); dcut_workspace_bytes() gives the
  *     size.
- *   - Calls are asynchronous on `stream` and never synchronise the host.  They
- *     keep no state between calls, with one exception: dcut_profile_arm sets a
- *     per-thread timing hook that later launches from the same host thread
- *     honour until it is disarmed (it records events only; results never
- *     depend on it).  Argument errors a host can see (sizes, limits, null
+ *   - Calls are asynchronous on `stream` and never synchronise the host.  No
+ *     result depends on an earlier call.  State the library does keep:
+ *     dcut_profile_arm sets a per-thread timing hook that later launches from
+ *     the same host thread honour until it is disarmed (it records events
+ *     only); the host side memoises the device's CU count and, per host thread,
+ *     each kernel's dynamic-LDS attribute; dcut_lm_head_argmax_static works in
+ *     a static device array of its own (see its declaration).  Argument errors a host can see (sizes, limits, null
  *     pointers, budgets, costs, operand spans) are rejected before any launch
  *     with DCUT_EINVAL or DCUT_EUNSUPPORTED; a failed launch returns DCUT_EHIP.
  *   - Faults in device-resident data never abort: they OR a DCUT_DERR_* bit
