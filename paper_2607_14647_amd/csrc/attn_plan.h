@@ -44,28 +44,30 @@ __device__ __forceinline__ int n_chunks(int L, int chunk, int MC) {
 
 // LDS of attn_plan_block for B requests and NT threads.
 inline size_t attn_plan_lds_bytes(int B, int NT) {
-  return (size_t)(((B + 3) & ~3) + 8 * B + 3 * (NT / 64)) * sizeof(int);
+  return (size_t)(((B + 3) & ~3) + 3 * (NT / 64)) * sizeof(int);
 }
 
 // The plan, built by one workgroup of NT threads (B <= PLAN_MAX_B); thread t
-// owns requests t*R .. t*R+R-1, R = ceil(B / NT).  Also reports capacity
-// faults of requests with kept rows.  `s` is attn_plan_lds_bytes(B, NT) of LDS.
+// owns requests t*R .. t*R+R-1, R = ceil(B / NT), and writes their items at
+// the places the order gives them: its full chunks after the full chunks of
+// the requests before it (a scan), its last chunk at its rank among the last
+// chunks (a count of larger keys).  Also reports capacity faults of requests
+// with kept rows.  `s` is attn_plan_lds_bytes(B, NT) of LDS.
 template <int NT>
 __device__ __forceinline__ void attn_plan_block(const AttnArgs &a, int *s) {
   constexpr int NW = NT / 64, RMAX = PLAN_MAX_B / NT;
   const int B = a.B, CH = a.chunk, MC = a.max_chunks, nkv = a.n_kv;
   const int B4 = (B + 3) & ~3;
   const int R = (B + NT - 1) / NT;
-  int *s_ck = s, *s_inv = s_ck + B4, *s_pre = s_inv + B, *s_t0 = s_pre + B, *s_d = s_t0 + B;
-  int *s_L = s_d + B, *s_cap = s_L + B, *s_last = s_cap + B, *s_w = s_last + B;
+  int *s_ck = s, *s_w = s_ck + B4;
   const int t = threadIdx.x, w = t >> 6, ln = t & 63;
-  int ck[RMAX], full[RMAX];
+  int ck[RMAX], full[RMAX], t0s[RMAX], ds[RMAX], Ls[RMAX], caps[RMAX], lasts[RMAX];
   int sum = 0, nl = 0, nv = 0;
 #pragma unroll
   for (int r = 0; r < RMAX; ++r) {
     const int j = t * R + r;
     int key = -1;
-    full[r] = 0;
+    full[r] = t0s[r] = ds[r] = Ls[r] = caps[r] = lasts[r] = 0;
     if (r < R && j < B) {
       const int t0 = a.cu[j];
       const int d = a.cu[j + 1] - t0;
@@ -78,7 +80,7 @@ __device__ __forceinline__ void attn_plan_block(const AttnArgs &a, int *s) {
         key = min(L + d - (nc - 1) * CH, 1 << 20);   // only a cap beyond max_ctx makes it larger
         full[r] = nc - 1;
       }
-      s_t0[j] = t0; s_d[j] = d; s_L[j] = L; s_cap[j] = cap; s_last[j] = nc - 1;
+      t0s[r] = t0; ds[r] = d; Ls[r] = L; caps[r] = cap; lasts[r] = nc - 1;
     }
     // sort key: length descending, then request index ascending (key <= 2^20,
     // B <= 1024), so a request's rank is the number of larger keys
@@ -114,52 +116,38 @@ __device__ __forceinline__ void attn_plan_block(const AttnArgs &a, int *s) {
     n_long += s_w[NW + v];
     n_live += s_w[2 * NW + v];
   }
+  const int e1 = n_long * nkv, e2 = e1 + n_full * nkv, e3 = e2 + (n_live - n_long) * nkv;
+  int32_t *plan = a.plan;
+  if (t == 0) plan[0] = e3;
+  int4 *items = (int4 *)((char *)plan + PLAN_HEAD);
   int run = before + x - sum;                     // full chunks of the requests before mine
   const int4 *k4 = (const int4 *)s_ck;
 #pragma unroll
   for (int r = 0; r < RMAX; ++r) {
     const int j = t * R + r;
-    if (r < R && j < B) {
-      s_pre[j] = run * nkv;
-      run += full[r];
-    }
-    if (r < R && ck[r] >= 0) {
-      int rank = 0;
+    if (r >= R || j >= B) continue;
+    const int pre = e1 + run * nkv;               // this request's first full-chunk item
+    run += full[r];
+    if (ck[r] < 0) continue;                      // no kept rows: no items
+    int rank = 0;
 #pragma unroll 4
-      for (int k = 0; k < (B4 >> 2); ++k) {
-        const int4 v = k4[k];
-        rank += (v.x > ck[r]) + (v.y > ck[r]) + (v.z > ck[r]) + (v.w > ck[r]);
-      }
-      s_inv[rank] = j;
+    for (int k = 0; k < (B4 >> 2); ++k) {
+      const int4 v = k4[k];
+      rank += (v.x > ck[r]) + (v.y > ck[r]) + (v.z > ck[r]) + (v.w > ck[r]);
     }
-  }
-  __syncthreads();
-  // consecutive threads write consecutive items
-  const int e1 = n_long * nkv, e2 = e1 + n_full * nkv, e3 = e2 + (n_live - n_long) * nkv;
-  int32_t *plan = a.plan;
-  if (t == 0) plan[0] = e3;
-  int4 *items = (int4 *)((char *)plan + PLAN_HEAD);
-  for (int p = t; p < e3; p += NT) {
-    int i, g, c;
-    if (p < e1 || p >= e2) {
-      const int r = p < e1 ? p / nkv : n_long + (p - e2) / nkv;
-      i = s_inv[r];
-      g = (p < e1 ? p : p - e2) % nkv;
-      c = s_last[i];
-    } else {
-      // the last request whose first full-chunk item is at or before f
-      const int f = p - e1;
-      int lo = 0, hi = B;
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (s_pre[mid] <= f) lo = mid; else hi = mid;
+    const int4 tail = make_int4(ds[r], Ls[r], caps[r], 0);
+    for (int c = 0; c < full[r]; ++c)
+      for (int g = 0; g < nkv; ++g) {
+        const int p = pre + c * nkv + g;
+        items[2 * p] = make_int4(j, g, c, t0s[r]);
+        items[2 * p + 1] = tail;
       }
-      i = lo;
-      c = (f - s_pre[i]) / nkv;
-      g = (f - s_pre[i]) % nkv;
+    // last chunks: the n_long longer than a chunk first, the others after the full chunks
+    const int base = rank < n_long ? rank * nkv : e2 + (rank - n_long) * nkv;
+    for (int g = 0; g < nkv; ++g) {
+      items[2 * (base + g)] = make_int4(j, g, lasts[r], t0s[r]);
+      items[2 * (base + g) + 1] = tail;
     }
-    items[2 * p] = make_int4(i, g, c, s_t0[i]);
-    items[2 * p + 1] = make_int4(s_d[i], s_L[i], s_cap[i], 0);
   }
 }
 
