@@ -197,7 +197,8 @@ __host__ __device__ inline bool lm_head_mid_tile(int M) { return M > 0 && M % 25
 // rows take the 256 x 256 tile, *mid when they take the 128 x 256 one (equal
 // when the launch makes no such choice).  The row stride must hold the larger.
 void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid);
-// split-K factor for a residual GEMM of this shape (a function of the shapes, never of K*)
+// split-K factor for a residual GEMM of this shape (a function of the shapes and the CU count,
+// never of K*)
 int gemm_splits(int M_max, int N, int K);
 // Whether the GEMM kernel's 32-bit buffer offsets reach every operand element:
 // a_rows rows of A at stride lda (what one task addresses: a row tile of at

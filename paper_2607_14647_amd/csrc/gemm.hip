@@ -789,17 +789,38 @@ int launch_epi(int kid, const GemmArgs &a, hipStream_t s) {
 }  // namespace
 
 int gemm_splits(int M_max, int N, int K) {
-  // sized for at most 1024 rows: a large batch verifies far fewer than its
-  // B(D+1) rows at the budgets a cost row picks (a quarter of them is common),
-  // and splits sized for B(D+1) would leave most CUs idle there
-  const int M_ref = M_max < 1024 ? M_max : 1024;
-  const int nMT = (M_ref + Small::TM - 1) / Small::TM, nNT = (N + Small::TN - 1) / Small::TN;
-  const int nk = (K + TK - 1) / TK;
-  int sp = (1024 + nMT * nNT - 1) / (nMT * nNT);
-  const int cap = nk / 16 > 1 ? nk / 16 : 1;    // keep at least 16 k-slices per split
-  if (sp > cap) sp = cap;
-  if (sp > 16) sp = 16;
-  return sp < 1 ? 1 : sp;
+  // Split-K tasks are Small tiles (128 x 128) over a k range, at most PER_CU of them per CU, and a
+  // split-K GEMM at few live rows runs at the per-CU load rate: its time is that of the busiest
+  // CU.  The factor minimises a model of that time summed over a quarter, a half, three quarters
+  // and all of M_ref = min(M_max, 1024) live rows (a large batch verifies far fewer than its
+  // B(D+1) rows at the budgets a cost row picks): the busiest CU's task count (tasks over CUs,
+  // rounded up) times a task's operand bytes, its float32 partial tile and a fixed cost per task
+  // (prologue and drain) worth about 150 KB of operand loads.  At least 16 k-slices per split;
+  // ties go to fewer splits.  The shapes and the CU count decide it, never the live rows.
+  const long long M_ref = M_max < 1024 ? M_max : 1024;
+  const long long nNT = (N + Small::TN - 1) / Small::TN, nk = (K + TK - 1) / TK;
+  long long cap = nk / 16;
+  if (cap > 16) cap = 16;
+  if (cap < 1) cap = 1;
+  const long long cus = cu_count();
+  int best = 1;
+  double best_cost = 0.0;
+  for (int sp = 1; sp <= cap; ++sp) {
+    const long long per = (nk + sp - 1) / sp;
+    const double bytes = (double)(Small::TM + Small::TN) * per * TK * 2 +
+                         (sp > 1 ? (double)Small::TM * Small::TN * 4 : 0.0) + 150e3;
+    double cost = 0.0;
+    for (int q = 1; q <= 4; ++q) {
+      const long long M = M_ref * q / 4 > 0 ? M_ref * q / 4 : 1;
+      const long long tasks = (M + Small::TM - 1) / Small::TM * nNT * sp;
+      cost += (double)((tasks + cus - 1) / cus) * bytes;
+    }
+    if (sp == 1 || cost < best_cost) {
+      best = sp;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 void gemm_argmax_slots(const GemmArgs &a, EpiKind epi, int *big, int *mid) {
